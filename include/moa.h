@@ -1,0 +1,198 @@
+/*
+ * moa.h -- C ABI of the MI355X (gfx950) ragged mixture-of-agents generation engine.
+ *
+ * What it computes. The paper's workload (Section "Problem Setting") is a
+ * fixed batch of pre-routed model calls: every (query, expert) pair chosen by
+ * the upstream router is an independent generation by that expert, and the
+ * aggregator call (Section "MOSAIC: Adaptive Aggregation", Eq. 11) is one more
+ * generation on the query followed by the expert outputs. Generation length
+ * drives the cost (Section "Workload Characterisation"), and decode is bound
+ * by memory bandwidth once a few prompts are in flight (appendix "Pitfalls of
+ * Data Concurrency and Over-Sharding"). This engine keeps every model
+ * co-resident on one GPU, shares one paged KV pool between them, and runs all
+ * models' requests in one ragged continuous batch per step: each call
+ * greedily decodes exactly max_new_tokens tokens (no end-of-sequence token).
+ *
+ * Conventions for every call:
+ *   - returns moa_status; MOA_OK == 0, errors are negative; no exception or
+ *     signal crosses the ABI;
+ *   - pointers named host_* / tokens / res / tok_buf are host memory, copied
+ *     before the call returns (the caller keeps ownership);
+ *   - dev_arena is device memory owned by the caller; the engine
+ *     sub-allocates weights, the KV pool and its workspace inside it and never
+ *     calls hipMalloc after moa_create; the arena and the stream must outlive
+ *     the engine;
+ *   - all device work is enqueued on the caller's stream;
+ *   - single host thread: an engine is not thread-safe;
+ *   - after MOA_EHIP only moa_destroy is valid on that engine.
+ */
+#ifndef MOA_H
+#define MOA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOA_OK = 0,
+  MOA_EINVAL = -1, /* bad argument (shape, id, length, capacity) */
+  MOA_ENOMEM = -2, /* arena, token store or block-list store too small */
+  MOA_ENOSPC = -3, /* request can never fit the KV pool */
+  MOA_ESTATE = -4, /* call not valid in the engine's current state */
+  MOA_EHIP = -5    /* HIP runtime error; the engine is unusable */
+} moa_status;
+
+enum { MOA_F32 = 0, MOA_BF16 = 1 };
+
+/* flags */
+enum {
+  /* Scheduler dry run: every call does its host bookkeeping but no device
+   * work is enqueued and no tokens are computed (collected tokens read -1).
+   * dev_arena and hip_stream may be NULL. */
+  MOA_FLAG_PLAN_ONLY = 1
+};
+
+/* Decoder geometry (Llama-style pre-norm decoder: RMSNorm, GQA attention with
+ * rotate-half RoPE, SwiGLU MLP, untied LM head). */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rope_theta, rms_eps;
+} moa_model_cfg;
+
+typedef struct {
+  moa_model_cfg model;        /* geometry shared by every model of the engine */
+  int32_t dtype;              /* MOA_F32 or MOA_BF16: weights, activations, KV */
+  int32_t kv_block_size;      /* token slots per KV block; must be 16 */
+  int32_t num_kv_blocks;      /* blocks in the shared KV pool (all layers) */
+  int32_t max_num_seqs;       /* running requests at once */
+  int32_t max_prefill_tokens; /* prompt tokens processed per step */
+  int32_t max_model_len;      /* max prompt + generated tokens of a request */
+  int32_t max_models;         /* models the arena reserves room for */
+  int32_t flags;              /* MOA_FLAG_* */
+  int64_t token_store;        /* device slots for prompt+output tokens of live requests (0: default) */
+  int64_t block_store;        /* device slots for block lists of live requests (0: default) */
+} moa_engine_cfg;
+
+typedef struct moa_engine moa_engine;
+
+typedef struct {
+  int64_t step;            /* index of the step just enqueued; -1: nothing to run */
+  int32_t admitted;        /* requests admitted this step */
+  int32_t prefill_tokens;  /* prompt positions processed */
+  int32_t decode_rows;     /* decode positions processed */
+  int32_t finished;        /* requests retired this step */
+  int32_t running;         /* running after the step */
+  int32_t pending;         /* waiting for admission after the step */
+  int32_t free_blocks;     /* free KV blocks after the step */
+} moa_step_info;
+
+typedef struct {
+  int64_t request_id;
+  int32_t model_id;
+  int32_t n_tokens;        /* == max_new_tokens of the request */
+  int64_t tok_offset;      /* where its tokens start in the caller's tok_buf */
+  int64_t finish_step;     /* step at which it retired */
+} moa_result;
+
+/* Device bytes moa_create + max_models moa_load_expert calls need in the arena.
+ * EINVAL: inconsistent cfg. */
+moa_status moa_arena_bytes(const moa_engine_cfg* cfg, size_t* bytes);
+
+/* Create an engine. cfg is copied. Lays out the KV pool and workspace inside
+ * dev_arena (arena_bytes >= moa_arena_bytes()). hip_stream is a hipStream_t.
+ * EINVAL: bad cfg (kv_block_size != 16, head_dim not 64/128 in bf16 mode,
+ * n_heads not a multiple of n_kv_heads, non-positive sizes). ENOMEM: arena too
+ * small. EHIP: runtime failure (no engine is returned). */
+moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_bytes,
+                      void* hip_stream, moa_engine** out);
+
+/* Load one model. host_weights is the packed blob: tensors in the order
+ *   embed[V,d], { attn_norm[d], wq[nh*hd,d], wk[nkv*hd,d], wv[nkv*hd,d],
+ *   wo[d,nh*hd], mlp_norm[d], w_gate[ffn,d], w_up[ffn,d], w_down[d,ffn] } x L,
+ *   final_norm[d], lm_head[V,d]
+ * each row-major [out, in], elements in the engine dtype (fp32, or bf16 bits),
+ * no padding. The engine re-lays the matrices out for its kernels. Model ids
+ * are dense, in load order; the aggregator is just another model. Blocks
+ * until the weights are resident. EINVAL: cfg differs from the engine's
+ * geometry or nbytes is wrong. ENOMEM: more than max_models. ESTATE: called
+ * after the first moa_step. */
+moa_status moa_load_expert(moa_engine* e, const moa_model_cfg* cfg, const void* host_weights,
+                           size_t nbytes, int32_t* model_id);
+
+/* Queue one generation call: prompt tokens[0..n_tokens) for model model_id,
+ * emitting exactly max_new_tokens tokens. Request ids are dense and increase
+ * in submit order. The request waits in a FIFO until its KV blocks
+ * ceil((n_tokens + max_new_tokens - 1) / 16) and a seat are free.
+ * EINVAL: n_tokens < 1, max_new_tokens < 1, unknown model, token id outside
+ * [0, vocab) (not checked in a MOA_FLAG_PLAN_ONLY dry run), n_tokens +
+ * max_new_tokens - 1 > max_model_len, or max_prefill_tokens == 0.
+ * ENOSPC: the request needs more blocks than the pool has.
+ * ENOMEM: token or block-list store full (collect finished requests first). */
+moa_status moa_submit(moa_engine* e, const int32_t* tokens, int32_t n_tokens, int32_t model_id,
+                      int32_t max_new_tokens, int64_t* request_id);
+
+/* Plan one step on the host and enqueue its kernels on the stream:
+ *   1 admit FIFO heads while a seat and their blocks are free (head-of-line
+ *     blocking); a request gets the smallest free block ids, ascending;
+ *   2 prefill: running requests in admission order take prompt positions up
+ *     to the per-step budget; completing a prompt emits token 0;
+ *   3 decode: every other running request with tokens left feeds its last
+ *     token and emits the next one;
+ *   4 retire requests that have emitted all tokens; their blocks are freed.
+ * Does not wait for the device (the sampled tokens stay on the device and feed
+ * the next step). info may be NULL; info->step == -1 when nothing is queued
+ * or running. EHIP on a runtime failure. */
+moa_status moa_step(moa_engine* e, moa_step_info* info);
+
+/* Return requests retired at steps <= upto_step (upto_step < 0: every step
+ * enqueued so far) that were not collected yet, in retirement order (step,
+ * then admission order), waiting for that step to finish on the device.
+ * Tokens are written back to back into tok_buf. If cap or tok_cap is too
+ * small nothing is drained, *n_out is set to the number of results that are
+ * ready and EINVAL is returned. */
+moa_status moa_collect(moa_engine* e, int64_t upto_step, moa_result* res, int32_t cap,
+                       int32_t* n_out, int32_t* tok_buf, int64_t tok_cap);
+
+/* Wait for every enqueued step. */
+moa_status moa_sync(moa_engine* e);
+
+void moa_destroy(moa_engine* e);
+const char* moa_status_str(moa_status s);
+
+/* ---- inspection hooks (tests) ---- */
+
+typedef struct {
+  int32_t model_id, prompt_len, max_new_tokens, n_blocks;
+  int64_t admit_step, finish_step; /* -1 until it happens */
+  int32_t n_chunks;                /* prefill chunks so far */
+  int32_t state;                   /* 0 pending, 1 running, 2 retired, 3 collected */
+} moa_request_info;
+
+moa_status moa_debug_request(moa_engine* e, int64_t request_id, moa_request_info* info);
+
+/* The request's KV block ids (ascending, as admitted). n_out = count. */
+moa_status moa_debug_block_table(moa_engine* e, int64_t request_id, int32_t* out, int32_t cap,
+                                 int32_t* n_out);
+
+/* The request's prefill chunks as (step, start, length) triples. */
+moa_status moa_debug_chunks(moa_engine* e, int64_t request_id, int64_t* out, int32_t cap_triples,
+                            int32_t* n_out);
+
+/* Per-step bookkeeping rows (step, admitted, prefill_tokens, decode_rows,
+ * finished, free_blocks_after), 6 int64 per step, oldest first. */
+moa_status moa_debug_steps(moa_engine* e, int64_t* out, int64_t cap_steps, int64_t* n_out);
+
+/* Capture the fp32 logits row of every token request_id emits: row j (the
+ * logits that produced output token j) is copied to host_logits + j * vocab
+ * once the step that computes it completes. host_logits must hold
+ * max_new_tokens * vocab floats and stay valid until the request is
+ * collected. Must be registered before the request's prefill completes. */
+moa_status moa_debug_capture_logits(moa_engine* e, int64_t request_id, float* host_logits);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOA_H */

@@ -23,9 +23,9 @@ head floor(h / (n_heads / n_kv_heads))), rotate-half RoPE with angles
 pos * theta^(-2i/head_dim), and argmax with ties broken to the lowest id.
 
 All arithmetic is float64 (weights are upcast from their fp32 or bf16
-storage). ``emulate_bf16=True`` additionally rounds to bf16 (nearest-even)
-at the points where a bf16 engine stores a value in bf16: the normed GEMM
-inputs, q/k/v after RoPE, the attention output and the SwiGLU output.
+storage). ``bf16_kv=True`` models a model state whose KV cache is stored in
+bf16: k (after RoPE) and v are rounded to bf16 (nearest-even) when they are
+written to the cache, exactly once; everything else stays float64.
 
 Parity pins (tests/test_oracle_*.py): single-key attention returns V, equal
 keys average V, softmax rows sum to 1, RoPE is the identity at position 0 and
@@ -176,14 +176,14 @@ class PagedKV:
         return K, V
 
 
-def forward_chunk(model, tokens, start, kv, emulate_bf16=False, want="all"):
+def forward_chunk(model, tokens, start, kv, bf16_kv=False, want="all"):
     """Run positions [start, start + len(tokens)) through the model, appending
     their K/V to ``kv`` (whose first ``start`` positions must already hold the
     history). Each position attends causally to positions <= itself.
     Returns logits [len(tokens), vocab] (``want="last"``: only the last row)."""
     m = model.shape
     n_h, n_kv, hd = m.n_heads, m.n_kv_heads, m.head_dim
-    rnd = bf16_round if emulate_bf16 else (lambda a: a)
+    store = bf16_round if bf16_kv else (lambda a: a)
     toks = np.asarray(tokens, dtype=np.int64)
     T = toks.shape[0]
     pos = np.arange(start, start + T)
@@ -192,55 +192,55 @@ def forward_chunk(model, tokens, start, kv, emulate_bf16=False, want="all"):
     x = E[toks].copy()
     for l in range(model.n_layers):
         p = f"layers.{l}."
-        xn = rnd(rmsnorm(x, model.W(p + "attn_norm"), m.rms_eps))
+        xn = rmsnorm(x, model.W(p + "attn_norm"), m.rms_eps)
         q = (xn @ model.W(p + "wq").T).reshape(T, n_h, hd)
         k = (xn @ model.W(p + "wk").T).reshape(T, n_kv, hd)
         v = (xn @ model.W(p + "wv").T).reshape(T, n_kv, hd)
-        q = rnd(apply_rope(q, cos, sin))
-        k = rnd(apply_rope(k, cos, sin))
-        v = rnd(v)
+        q = apply_rope(q, cos, sin)
+        k = store(apply_rope(k, cos, sin))
+        v = store(v)
         kv.write(l, start, k, v)
         K, V = kv.read(l, start + T)
         att = np.empty((T, n_h, hd))
         for t in range(T):
             att[t] = attend(q[t], K[: start + t + 1], V[: start + t + 1])
-        att = rnd(att.reshape(T, n_h * hd))
+        att = att.reshape(T, n_h * hd)
         h = x + att @ model.W(p + "wo").T
-        hn = rnd(rmsnorm(h, model.W(p + "mlp_norm"), m.rms_eps))
+        hn = rmsnorm(h, model.W(p + "mlp_norm"), m.rms_eps)
         g = hn @ model.W(p + "w_gate").T
         u = hn @ model.W(p + "w_up").T
-        a = rnd(silu(g) * u)
+        a = silu(g) * u
         x = h + a @ model.W(p + "w_down").T
     if want == "last":
         x = x[-1:]
-    xf = rnd(rmsnorm(x, model.W("final_norm"), m.rms_eps))
+    xf = rmsnorm(x, model.W("final_norm"), m.rms_eps)
     return xf @ model.W("lm_head").T
 
 
-def forward_full(model, tokens, emulate_bf16=False):
+def forward_full(model, tokens, bf16_kv=False):
     """Logits at every position of ``tokens`` computed from scratch (no prior cache)."""
     kv = ContiguousKV(model.n_layers, model.shape.n_kv_heads, model.shape.head_dim)
-    return forward_chunk(model, tokens, 0, kv, emulate_bf16)
+    return forward_chunk(model, tokens, 0, kv, bf16_kv)
 
 
-def brute_force_prefix_logits(model, tokens, emulate_bf16=False):
+def brute_force_prefix_logits(model, tokens, bf16_kv=False):
     """Logits at position t recomputed from tokens[0..t] alone, for every t
     (quadratic cost; tiny inputs only)."""
-    return np.stack([forward_full(model, tokens[: t + 1], emulate_bf16)[-1]
+    return np.stack([forward_full(model, tokens[: t + 1], bf16_kv)[-1]
                      for t in range(len(tokens))])
 
 
-def greedy_generate(model, prompt, G, kv=None, emulate_bf16=False, return_logits=False):
+def greedy_generate(model, prompt, G, kv=None, bf16_kv=False, return_logits=False):
     """Greedy decoding of exactly G tokens (no end-of-sequence token).
     The prompt is prefilled in one chunk; each later token is one decode step."""
     m = model.shape
     if kv is None:
         kv = ContiguousKV(model.n_layers, m.n_kv_heads, m.head_dim)
     P = len(prompt)
-    lg = forward_chunk(model, prompt, 0, kv, emulate_bf16, want="last")[-1]
+    lg = forward_chunk(model, prompt, 0, kv, bf16_kv, want="last")[-1]
     out, logits = [argmax_lowest(lg)], [lg]
     for j in range(1, G):
-        lg = forward_chunk(model, [out[-1]], P + j - 1, kv, emulate_bf16)[-1]
+        lg = forward_chunk(model, [out[-1]], P + j - 1, kv, bf16_kv)[-1]
         out.append(argmax_lowest(lg))
         logits.append(lg)
     if return_logits:
@@ -248,16 +248,16 @@ def greedy_generate(model, prompt, G, kv=None, emulate_bf16=False, return_logits
     return out
 
 
-def teacher_forced_logits(model, prompt, outputs, emulate_bf16=False):
+def teacher_forced_logits(model, prompt, outputs, bf16_kv=False):
     """Logits that produce each of ``outputs`` when the history is the prompt
     followed by the given outputs (so a flip never cascades): rows are the
     positions P-1 .. P+G-2 of prompt ++ outputs[:-1]."""
     seq = np.concatenate([np.asarray(prompt, dtype=np.int64),
                           np.asarray(outputs[:-1], dtype=np.int64)])
-    return forward_full(model, seq, emulate_bf16)[len(prompt) - 1:]
+    return forward_full(model, seq, bf16_kv)[len(prompt) - 1:]
 
 
-def decode_from_history(model, K_hist, V_hist, token, pos, emulate_bf16=False):
+def decode_from_history(model, K_hist, V_hist, token, pos, bf16_kv=False):
     """One decode step for a sequence whose K/V at positions [0, pos) is given
     (per layer [pos, n_kv, hd]); returns the logits of ``token`` at ``pos``."""
     m = model.shape
@@ -265,4 +265,4 @@ def decode_from_history(model, K_hist, V_hist, token, pos, emulate_bf16=False):
     for l in range(model.n_layers):
         kv.K[l] = np.asarray(K_hist[l], dtype=np.float64)
         kv.V[l] = np.asarray(V_hist[l], dtype=np.float64)
-    return forward_chunk(model, [token], pos, kv, emulate_bf16)[-1]
+    return forward_chunk(model, [token], pos, kv, bf16_kv)[-1]

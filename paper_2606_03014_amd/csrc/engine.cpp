@@ -1,0 +1,986 @@
+// Host side of the ragged MoA generation engine: request table, FIFO
+// admission, paged-KV block allocator, step planner, metadata upload and the
+// per-step kernel sequence. See include/moa.h for the contract.
+#include "moa.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <array>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <new>
+#include <thread>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace moa;
+
+namespace {
+
+constexpr int kStageSlots = 4;    // steps that may be in flight (pinned staging ring)
+constexpr int kTargetWaves = 4096;
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+struct Request {
+  int64_t id = 0;
+  int32_t model = 0, P = 0, G = 0, need = 0;
+  int32_t pre = 0, gen = 0;
+  bool fresh = false;
+  int64_t tok_off = -1;               // token store: P prompt slots, then G outputs
+  int64_t bt_off = -1;                // block store: need entries
+  std::vector<int32_t> blocks;
+  std::vector<int32_t> prompt;        // host copy until uploaded at admission
+  int64_t admit_step = -1, finish_step = -1;
+  std::vector<std::array<int64_t, 3>> chunks;
+  int state = 0;                      // 0 pending, 1 running, 2 retired, 3 collected
+  float* capture = nullptr;
+};
+
+struct ModelDev {
+  // device pointers (bf16 bits or f32)
+  const void* embed = nullptr;
+  std::vector<const void*> attn_norm, wqkv, wo, mlp_norm, wgu, wdown;
+  const void* final_norm = nullptr;
+  const void* lm_head = nullptr;
+};
+
+// Free-block set: bit i set <=> block i free. take() returns the k smallest.
+struct BlockSet {
+  std::vector<uint64_t> bits;
+  int64_t nfree = 0;
+  size_t lo = 0;   // no free bit below word lo
+  void init(int64_t n) {
+    bits.assign((n + 63) / 64, 0);
+    for (int64_t i = 0; i < n; ++i) bits[i >> 6] |= 1ull << (i & 63);
+    nfree = n;
+    lo = 0;
+  }
+  void take(int32_t k, std::vector<int32_t>& out) {
+    out.clear();
+    out.reserve(k);
+    size_t w = lo;
+    while ((int32_t)out.size() < k) {
+      uint64_t v = bits[w];
+      while (v && (int32_t)out.size() < k) {
+        int b = __builtin_ctzll(v);
+        v &= v - 1;
+        out.push_back((int32_t)(w * 64 + b));
+      }
+      if ((int32_t)out.size() < k) ++w;
+    }
+    for (int32_t b : out) bits[b >> 6] &= ~(1ull << (b & 63));
+    nfree -= k;
+    while (lo < bits.size() && bits[lo] == 0) ++lo;
+  }
+  void give(const std::vector<int32_t>& v) {
+    for (int32_t b : v) {
+      bits[b >> 6] |= 1ull << (b & 63);
+      if ((size_t)(b >> 6) < lo) lo = b >> 6;
+    }
+    nfree += (int64_t)v.size();
+  }
+};
+
+struct Layout {
+  size_t esz;
+  int64_t Tmax, Rmax, slots_cap, items_cap, red_cap, part_cap;
+  size_t model_bytes, kv_bytes, block_bytes;
+  size_t off_kv, off_tok, off_bt, off_rope, off_meta, off_x, off_xn, off_part, off_q, off_ao, off_h,
+      off_logits, off_pacc, off_pml, off_models, total;
+  int64_t token_store, block_store, meta_ints;
+};
+
+bool valid_cfg(const moa_engine_cfg& c) {
+  const moa_model_cfg& m = c.model;
+  if (c.dtype != MOA_F32 && c.dtype != MOA_BF16) return false;
+  if (c.kv_block_size != kBlock) return false;
+  if (m.n_layers < 1 || m.d_model < 32 || m.n_heads < 1 || m.n_kv_heads < 1 || m.vocab < 1 || m.ffn_dim < 32)
+    return false;
+  if (m.n_heads % m.n_kv_heads) return false;
+  const int gq = m.n_heads / m.n_kv_heads;
+  if (gq != 1 && gq != 2 && gq != 4 && gq != 8) return false;
+  if (m.head_dim != 64 && m.head_dim != 128) return false;
+  if (!(m.rms_eps > 0.f) || !(m.rope_theta > 0.f)) return false;
+  if (m.d_model % 64 || m.ffn_dim % 64 || m.vocab % 16) return false;
+  if (c.dtype == MOA_F32 && (m.vocab % 64 || (2 * m.ffn_dim) % 64)) return false;
+  // bf16 GEMMs stream K in batches of 4 MFMA k-steps of 32
+  if (c.dtype == MOA_BF16 && (m.d_model % 128 || m.ffn_dim % 128 || (m.n_heads * m.head_dim) % 128)) return false;
+  if (c.num_kv_blocks < 1 || c.max_num_seqs < 1 || c.max_prefill_tokens < 0 || c.max_model_len < 2) return false;
+  if (c.max_models < 1 || c.max_models > kMaxModels) return false;
+  if (c.token_store < 0 || c.block_store < 0) return false;
+  return true;
+}
+
+Layout make_layout(const moa_engine_cfg& c) {
+  Layout L{};
+  const moa_model_cfg& m = c.model;
+  L.esz = c.dtype == MOA_BF16 ? 2 : 4;
+  const int64_t d = m.d_model, hd = m.head_dim, nh = m.n_heads, nkv = m.n_kv_heads, V = m.vocab,
+                F = m.ffn_dim, Lr = m.n_layers;
+  const int64_t qkv = (nh + 2 * nkv) * hd;
+  L.Tmax = (int64_t)c.max_prefill_tokens + c.max_num_seqs;
+  L.Rmax = c.max_num_seqs;
+  L.slots_cap = (int64_t)c.num_kv_blocks * kBlock / kSplitKeys + c.max_num_seqs + 1;
+  L.items_cap = L.Tmax + L.slots_cap;
+  L.red_cap = c.max_num_seqs;
+  int64_t pc = L.Tmax * std::max(qkv, d);
+  if (c.dtype == MOA_F32) pc = std::max(pc, L.Tmax * 2 * F);
+  L.part_cap = pc;
+  L.token_store = c.token_store ? c.token_store : (int64_t)64 << 20;
+  L.block_store = c.block_store ? c.block_store : (int64_t)16 << 20;
+  L.meta_ints = 4 * L.Tmax + 2 * L.Rmax + 4 * L.items_cap + 4 * L.red_cap;
+  L.block_bytes = (size_t)Lr * nkv * 2 * kBlock * hd * L.esz;
+  L.kv_bytes = L.block_bytes * (size_t)c.num_kv_blocks;
+  const size_t per_layer = (size_t)(2 * d + qkv * d + d * nh * hd + 3 * F * d) * L.esz;
+  L.model_bytes = align_up((size_t)(2 * V * d + d) * L.esz + 256 * (8 + 6 * Lr) + per_layer * Lr, 256);
+
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off = align_up(off + bytes, 256); return o; };
+  L.off_kv = take(L.kv_bytes);
+  L.off_tok = take((size_t)L.token_store * 4);
+  L.off_bt = take((size_t)L.block_store * 4);
+  L.off_rope = take((size_t)c.max_model_len * (hd / 2) * sizeof(float2));
+  L.off_meta = take((size_t)L.meta_ints * 4);
+  L.off_x = take((size_t)L.Tmax * d * 4);
+  // GEMM inputs (xn, ao, h) hold two planes: bf16 hi and lo (fp32 mode uses the first)
+  L.off_xn = take((size_t)2 * L.Tmax * d * L.esz);
+  L.off_part = take((size_t)L.part_cap * 4);
+  L.off_q = take((size_t)L.Tmax * nh * hd * 4);
+  L.off_ao = take((size_t)2 * L.Tmax * nh * hd * L.esz);
+  L.off_h = take((size_t)2 * L.Tmax * F * L.esz);
+  L.off_logits = take((size_t)L.Rmax * V * 4);
+  L.off_pacc = take((size_t)L.slots_cap * nh * hd * 4);
+  L.off_pml = take((size_t)L.slots_cap * nh * 2 * 4);
+  L.off_models = off;
+  L.total = off + L.model_bytes * (size_t)c.max_models;
+  return L;
+}
+
+}  // namespace
+
+struct moa_engine {
+  moa_engine_cfg cfg{};
+  Layout lay{};
+  bool plan_only = false;
+  bool bf16 = false;
+  bool broken = false;
+  hipStream_t stream = nullptr;
+  hipStream_t copy_stream = nullptr;
+  char* arena = nullptr;
+  size_t arena_bytes = 0;
+  size_t model_top = 0;
+
+  std::vector<ModelDev> models;
+  std::vector<Request> reqs;
+  std::deque<int64_t> pending;
+  std::vector<int64_t> running;
+  std::vector<int64_t> done;          // retired, not collected, in retirement order
+  BlockSet free_blocks;
+  int64_t tok_top = 0, bt_top = 0;
+  int64_t step_idx = 0;
+  int64_t live = 0;                   // requests not yet collected
+  std::vector<std::array<int64_t, 6>> trace;
+
+  // device views
+  char* kv = nullptr;
+  int* tok_store = nullptr;
+  int* bt_store = nullptr;
+  float2* rope = nullptr;
+  int* meta = nullptr;
+  float* x = nullptr;
+  void* xn = nullptr;
+  float* part = nullptr;
+  float* q = nullptr;
+  void* ao = nullptr;
+  void* h = nullptr;
+  float* logits = nullptr;
+  float* pacc = nullptr;
+  float* pml = nullptr;
+
+  // pinned staging ring and per-step completion events
+  struct Stage { char* buf = nullptr; size_t cap = 0; };
+  Stage stage[kStageSlots];
+  hipEvent_t ev[kStageSlots] = {};
+  int64_t ev_step[kStageSlots] = {-1, -1, -1, -1};
+  int32_t* pinned_out = nullptr;
+  size_t pinned_out_cap = 0;
+
+  // per-step host plan (reused vectors)
+  std::vector<int> r_tok, r_pos, r_bt, r_model, l_src, l_dst;
+  std::vector<AttnItem> items;
+  std::vector<ReduceItem> red;
+};
+
+namespace {
+
+moa_status hip_fail(moa_engine* e, hipError_t err, const char* what) {
+  if (e) e->broken = true;
+  std::fprintf(stderr, "moa: HIP error in %s: %s\n", what, hipGetErrorString(err));
+  return MOA_EHIP;
+}
+
+#define HIPCHK(call, what)                              \
+  do {                                                  \
+    hipError_t _err = (call);                           \
+    if (_err != hipSuccess) return hip_fail(e, _err, what); \
+  } while (0)
+
+// Tile-shuffle a row-major [N][K] bf16 matrix into MFMA B-fragment order:
+// fragment (n/16, k/32) is 64 lanes x 8 contiguous elements, lane = n%16 +
+// 16*((k%32)/8). Rows are taken from src_rows(n) so the gate/up interleave and
+// the q|k|v concatenation are done in the same pass.
+template <class RowFn>
+void shuffle_bf16(uint16_t* dst, int64_t N, int64_t K, RowFn src_row) {
+  const int64_t KS = K / 32, NT = N / 16;
+  auto work = [&](int64_t t0, int64_t t1) {
+    for (int64_t nt = t0; nt < t1; ++nt)
+      for (int r = 0; r < 16; ++r) {
+        const uint16_t* s = src_row(nt * 16 + r);
+        for (int64_t k = 0; k < K; ++k) {
+          const int64_t ks = k >> 5, kk = k & 31;
+          dst[((nt * KS + ks) * 64 + (r + 16 * (kk >> 3))) * 8 + (kk & 7)] = s[k];
+        }
+      }
+  };
+  unsigned nth = std::max(1u, std::min(16u, std::thread::hardware_concurrency()));
+  if (NT < 64) nth = 1;
+  std::vector<std::thread> th;
+  for (unsigned i = 0; i < nth; ++i) th.emplace_back(work, NT * i / nth, NT * (i + 1) / nth);
+  for (auto& t : th) t.join();
+}
+
+struct GemmPlanIn {
+  int ngroups = 0;
+  int row0[kMaxModels], nrows[kMaxModels];
+  const void* W[kMaxModels];
+};
+
+// Choose the tiling and k-split of one grouped GEMM and fill its arguments.
+// X is a split-bf16 pair (lo plane x_lo elements after hi) in bf16 mode.
+void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi, const void* X, size_t x_lo,
+               float* out, uint16_t* hout, size_t h_lo, bool allow_split, GemmArgs& a, int& mt, int& nt) {
+  std::memset(&a, 0, sizeof(a));
+  a.ngroups = in.ngroups;
+  a.X = X;
+  a.x_lo = x_lo;
+  a.h_lo = h_lo;
+  a.K = K;
+  a.N = N;
+  a.out = out;
+  a.hout = hout;
+  int maxM = 0, totalM = 0;
+  for (int g = 0; g < in.ngroups; ++g) { maxM = std::max(maxM, in.nrows[g]); totalM += in.nrows[g]; }
+  if (!e->bf16) {
+    mt = 1; nt = 1;
+    int item = 0;
+    for (int g = 0; g < in.ngroups; ++g) {
+      a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
+      a.g[g].n_mc = (in.nrows[g] + 15) / 16;
+      a.g[g].item0 = item;
+      item += a.g[g].n_mc * (N / 64);
+    }
+    a.S = 1; a.ksteps = 0; a.out_split = 0; a.total_items = item;
+    return;
+  }
+  mt = maxM <= 16 ? 1 : (maxM <= 32 ? 2 : 4);
+  nt = (epi == EPI_SWIGLU) ? 2 : 1;
+  const int tiles = N / 16 / nt;
+  const int KS = K / 32;
+  int base = 0;
+  for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 16 * mt - 1) / (16 * mt)) * tiles;
+  int S = 1;
+  if (allow_split) {
+    while (base * S < kTargetWaves && KS % (S * 2 * 8) == 0 &&
+           (int64_t)S * 2 * totalM * N <= e->lay.part_cap && S < 16)
+      S *= 2;
+  }
+  a.S = S;
+  a.ksteps = KS / S;
+  a.out_split = (size_t)totalM * N;  // partial s lives at out + s * rows * N
+  int item = 0;
+  for (int g = 0; g < in.ngroups; ++g) {
+    a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
+    a.g[g].n_mc = (in.nrows[g] + 16 * mt - 1) / (16 * mt);
+    a.g[g].item0 = item;
+    item += a.g[g].n_mc * S * tiles;
+  }
+  a.total_items = item;
+}
+
+}  // namespace
+
+// ==================================================================== C ABI
+
+extern "C" {
+
+const char* moa_status_str(moa_status s) {
+  switch (s) {
+    case MOA_OK: return "MOA_OK";
+    case MOA_EINVAL: return "MOA_EINVAL: invalid argument";
+    case MOA_ENOMEM: return "MOA_ENOMEM: arena or store too small";
+    case MOA_ENOSPC: return "MOA_ENOSPC: request can never fit the KV pool";
+    case MOA_ESTATE: return "MOA_ESTATE: call not valid in this state";
+    case MOA_EHIP: return "MOA_EHIP: HIP runtime error";
+  }
+  return "unknown moa_status";
+}
+
+moa_status moa_arena_bytes(const moa_engine_cfg* cfg, size_t* bytes) {
+  if (!cfg || !bytes || !valid_cfg(*cfg)) return MOA_EINVAL;
+  *bytes = make_layout(*cfg).total;
+  return MOA_OK;
+}
+
+moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_bytes, void* hip_stream,
+                      moa_engine** out) {
+  if (!cfg || !out || !valid_cfg(*cfg)) return MOA_EINVAL;
+  *out = nullptr;
+  const bool plan_only = (cfg->flags & MOA_FLAG_PLAN_ONLY) != 0;
+  Layout L = make_layout(*cfg);
+  if (!plan_only) {
+    if (!dev_arena) return MOA_EINVAL;
+    if (arena_bytes < L.total) return MOA_ENOMEM;
+    if (((uintptr_t)dev_arena) % 256) return MOA_EINVAL;
+  }
+  moa_engine* e = new (std::nothrow) moa_engine();
+  if (!e) return MOA_ENOMEM;
+  e->cfg = *cfg;
+  e->lay = L;
+  e->plan_only = plan_only;
+  e->bf16 = cfg->dtype == MOA_BF16;
+  e->free_blocks.init(cfg->num_kv_blocks);
+  e->model_top = L.off_models;
+  if (!plan_only) {
+    e->stream = (hipStream_t)hip_stream;
+    e->arena = (char*)dev_arena;
+    e->arena_bytes = arena_bytes;
+    char* A = e->arena;
+    e->kv = A + L.off_kv;
+    e->tok_store = (int*)(A + L.off_tok);
+    e->bt_store = (int*)(A + L.off_bt);
+    e->rope = (float2*)(A + L.off_rope);
+    e->meta = (int*)(A + L.off_meta);
+    e->x = (float*)(A + L.off_x);
+    e->xn = A + L.off_xn;
+    e->part = (float*)(A + L.off_part);
+    e->q = (float*)(A + L.off_q);
+    e->ao = A + L.off_ao;
+    e->h = A + L.off_h;
+    e->logits = (float*)(A + L.off_logits);
+    e->pacc = (float*)(A + L.off_pacc);
+    e->pml = (float*)(A + L.off_pml);
+    hipError_t err = hipStreamCreateWithFlags(&e->copy_stream, hipStreamNonBlocking);
+    for (int i = 0; i < kStageSlots && err == hipSuccess; ++i) err = hipEventCreateWithFlags(&e->ev[i], hipEventDisableTiming);
+    if (err == hipSuccess) {
+      // RoPE table: angle pos * theta^(-2i/hd) and its cos/sin in double, stored as fp32.
+      const int hd = cfg->model.head_dim, half = hd / 2;
+      std::vector<float2> tab((size_t)cfg->max_model_len * half);
+      for (int p = 0; p < cfg->max_model_len; ++p)
+        for (int i = 0; i < half; ++i) {
+          const double inv = std::pow((double)cfg->model.rope_theta, -(2.0 * i) / hd);
+          const double ang = (double)p * inv;
+          tab[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+        }
+      err = hipMemcpy(e->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
+    }
+    if (err != hipSuccess) {
+      hip_fail(nullptr, err, "moa_create");
+      moa_destroy(e);
+      return MOA_EHIP;
+    }
+  }
+  *out = e;
+  return MOA_OK;
+}
+
+void moa_destroy(moa_engine* e) {
+  if (!e) return;
+  if (!e->plan_only) {
+    if (e->stream) (void)hipStreamSynchronize(e->stream);
+    for (int i = 0; i < kStageSlots; ++i) {
+      if (e->stage[i].buf) (void)hipHostFree(e->stage[i].buf);
+      if (e->ev[i]) (void)hipEventDestroy(e->ev[i]);
+    }
+    if (e->pinned_out) (void)hipHostFree(e->pinned_out);
+    if (e->copy_stream) (void)hipStreamDestroy(e->copy_stream);
+  }
+  delete e;
+}
+
+moa_status moa_load_expert(moa_engine* e, const moa_model_cfg* mc, const void* host_weights, size_t nbytes,
+                           int32_t* model_id) {
+  if (!e || !mc || !host_weights || !model_id) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (e->step_idx > 0) return MOA_ESTATE;
+  const moa_model_cfg& g = e->cfg.model;
+  if (mc->n_layers != g.n_layers || mc->d_model != g.d_model || mc->n_heads != g.n_heads ||
+      mc->n_kv_heads != g.n_kv_heads || mc->head_dim != g.head_dim || mc->ffn_dim != g.ffn_dim ||
+      mc->vocab != g.vocab || mc->rope_theta != g.rope_theta || mc->rms_eps != g.rms_eps)
+    return MOA_EINVAL;
+  const size_t esz = e->lay.esz;
+  const int64_t d = g.d_model, hd = g.head_dim, nh = g.n_heads, nkv = g.n_kv_heads, V = g.vocab, F = g.ffn_dim,
+                Lr = g.n_layers;
+  const int64_t qd = nh * hd, kd = nkv * hd, qkv = qd + 2 * kd;
+  const size_t expect = (size_t)(2 * V * d + d + Lr * (2 * d + qkv * d + d * qd + 3 * F * d)) * esz;
+  if (nbytes != expect) return MOA_EINVAL;
+  if ((int)e->models.size() >= e->cfg.max_models) return MOA_ENOMEM;
+
+  ModelDev M;
+  if (e->plan_only) {
+    *model_id = (int32_t)e->models.size();
+    e->models.push_back(M);
+    return MOA_OK;
+  }
+  const char* src = (const char*)host_weights;
+  size_t so = 0;
+  auto next = [&](int64_t n) { const char* p = src + so; so += (size_t)n * esz; return p; };
+  size_t mo = e->model_top;
+  const size_t mend = mo + e->lay.model_bytes;
+  auto dev_take = [&](int64_t n) -> char* {
+    char* p = e->arena + mo;
+    mo = align_up(mo + (size_t)n * esz, 256);
+    return p;
+  };
+  std::vector<char> tmp;
+  auto put_raw = [&](const char* s, int64_t n) -> const void* {
+    char* p = dev_take(n);
+    if (hipMemcpy(p, s, (size_t)n * esz, hipMemcpyHostToDevice) != hipSuccess) return nullptr;
+    return p;
+  };
+  // matrix built from row sources (bf16: tile-shuffled; f32: row-major)
+  auto put_mat = [&](int64_t N, int64_t K, auto rowfn) -> const void* {
+    char* p = dev_take(N * K);
+    tmp.resize((size_t)N * K * esz);
+    if (e->bf16) {
+      shuffle_bf16((uint16_t*)tmp.data(), N, K, [&](int64_t n) { return (const uint16_t*)rowfn(n); });
+    } else {
+      for (int64_t n = 0; n < N; ++n) std::memcpy(tmp.data() + (size_t)n * K * esz, rowfn(n), (size_t)K * esz);
+    }
+    if (hipMemcpy(p, tmp.data(), tmp.size(), hipMemcpyHostToDevice) != hipSuccess) return nullptr;
+    return p;
+  };
+  bool ok = true;
+  auto chk = [&](const void* p) { if (!p) ok = false; return p; };
+  M.embed = chk(put_raw(next(V * d), V * d));
+  for (int64_t l = 0; l < Lr && ok; ++l) {
+    const char* an = next(d);
+    const char* wq = next(qd * d);
+    const char* wk = next(kd * d);
+    const char* wv = next(kd * d);
+    const char* wo = next(d * qd);
+    const char* mn = next(d);
+    const char* wg = next(F * d);
+    const char* wu = next(F * d);
+    const char* wd = next(d * F);
+    M.attn_norm.push_back(chk(put_raw(an, d)));
+    M.wqkv.push_back(chk(put_mat(qkv, d, [&](int64_t n) {
+      if (n < qd) return wq + (size_t)n * d * esz;
+      if (n < qd + kd) return wk + (size_t)(n - qd) * d * esz;
+      return wv + (size_t)(n - qd - kd) * d * esz;
+    })));
+    M.wo.push_back(chk(put_mat(d, qd, [&](int64_t n) { return wo + (size_t)n * qd * esz; })));
+    M.mlp_norm.push_back(chk(put_raw(mn, d)));
+    if (e->bf16) {
+      // 16-row tiles alternate gate / up so a wavefront owning tiles (2i, 2i+1)
+      // holds gate and up of the same hidden units.
+      M.wgu.push_back(chk(put_mat(2 * F, d, [&](int64_t n) {
+        const int64_t t = n / 16, r = n % 16, unit = (t / 2) * 16 + r;
+        return ((t & 1) ? wu : wg) + (size_t)unit * d * esz;
+      })));
+    } else {
+      M.wgu.push_back(chk(put_mat(2 * F, d, [&](int64_t n) {
+        return n < F ? wg + (size_t)n * d * esz : wu + (size_t)(n - F) * d * esz;
+      })));
+    }
+    M.wdown.push_back(chk(put_mat(d, F, [&](int64_t n) { return wd + (size_t)n * F * esz; })));
+  }
+  if (ok) M.final_norm = chk(put_raw(next(d), d));
+  if (ok) {
+    const char* lm = next(V * d);
+    M.lm_head = chk(put_mat(V, d, [&](int64_t n) { return lm + (size_t)n * d * esz; }));
+  }
+  if (!ok) return hip_fail(e, hipErrorUnknown, "moa_load_expert copy");
+  if (mo > mend || mo > e->arena_bytes) return hip_fail(e, hipErrorOutOfMemory, "moa_load_expert layout");
+  e->model_top = e->lay.off_models + e->lay.model_bytes * (e->models.size() + 1);
+  *model_id = (int32_t)e->models.size();
+  e->models.push_back(std::move(M));
+  return MOA_OK;
+}
+
+moa_status moa_submit(moa_engine* e, const int32_t* tokens, int32_t n_tokens, int32_t model_id,
+                      int32_t max_new_tokens, int64_t* request_id) {
+  if (!e || !request_id) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (!tokens || n_tokens < 1 || max_new_tokens < 1) return MOA_EINVAL;
+  if (model_id < 0 || model_id >= (int32_t)e->models.size()) return MOA_EINVAL;
+  if ((int64_t)n_tokens + max_new_tokens - 1 > e->cfg.max_model_len) return MOA_EINVAL;
+  if (e->cfg.max_prefill_tokens < 1) return MOA_EINVAL;     // a prompt could never be processed
+  if (!e->plan_only)   // a dry run never reads token values (its collected tokens are -1)
+    for (int32_t i = 0; i < n_tokens; ++i)
+      if (tokens[i] < 0 || tokens[i] >= e->cfg.model.vocab) return MOA_EINVAL;
+  const int64_t need = ((int64_t)n_tokens + max_new_tokens - 1 + kBlock - 1) / kBlock;
+  if (need > e->cfg.num_kv_blocks) return MOA_ENOSPC;
+  if (e->live == 0) e->tok_top = 0, e->bt_top = 0;    // stores are empty again: restart them
+  if (e->tok_top + n_tokens + max_new_tokens > e->lay.token_store) return MOA_ENOMEM;
+  Request r;
+  r.id = (int64_t)e->reqs.size();
+  r.model = model_id;
+  r.P = n_tokens;
+  r.G = max_new_tokens;
+  r.need = (int32_t)need;
+  r.tok_off = e->tok_top;
+  e->tok_top += (int64_t)n_tokens + max_new_tokens;
+  r.prompt.assign(tokens, tokens + n_tokens);
+  e->reqs.push_back(std::move(r));
+  e->pending.push_back(e->reqs.back().id);
+  e->live += 1;
+  *request_id = e->reqs.back().id;
+  return MOA_OK;
+}
+
+namespace {
+
+// Wait until staging slot `slot` is no longer read by an in-flight step.
+moa_status wait_slot(moa_engine* e, int slot) {
+  if (e->ev_step[slot] >= 0) HIPCHK(hipEventSynchronize(e->ev[slot]), "staging wait");
+  return MOA_OK;
+}
+
+moa_status ensure_stage(moa_engine* e, int slot, size_t bytes) {
+  auto& s = e->stage[slot];
+  if (s.cap >= bytes) return MOA_OK;
+  if (s.buf) HIPCHK(hipHostFree(s.buf), "hipHostFree");
+  s.buf = nullptr;
+  s.cap = 0;
+  size_t cap = std::max(bytes, (size_t)1 << 20);
+  HIPCHK(hipHostMalloc((void**)&s.buf, cap, hipHostMallocDefault), "hipHostMalloc");
+  s.cap = cap;
+  return MOA_OK;
+}
+
+moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int T, int R,
+                        const int* grp_rows, const int* grp_lm) {
+  const moa_model_cfg& g = e->cfg.model;
+  const Layout& L = e->lay;
+  const int slot = (int)(e->step_idx % kStageSlots);
+  moa_status st = wait_slot(e, slot);
+  if (st != MOA_OK) return st;
+
+  // ---- stage: metadata, then prompts and block lists of admitted requests
+  const int nitems = (int)e->items.size(), nred = (int)e->red.size();
+  size_t meta_ints = 4 * (size_t)T + 2 * (size_t)R + 4 * (size_t)nitems + 4 * (size_t)nred;
+  size_t up_ints = 0;
+  for (int64_t id : admitted) up_ints += e->reqs[id].prompt.size() + e->reqs[id].blocks.size();
+  st = ensure_stage(e, slot, (meta_ints + up_ints) * 4);
+  if (st != MOA_OK) return st;
+  int* hb = (int*)e->stage[slot].buf;
+  size_t o = 0;
+  auto put = [&](const void* p, size_t n_int) { std::memcpy(hb + o, p, n_int * 4); o += n_int; };
+  const size_t o_tok = o; put(e->r_tok.data(), T);
+  const size_t o_pos = o; put(e->r_pos.data(), T);
+  const size_t o_bt = o; put(e->r_bt.data(), T);
+  const size_t o_mod = o; put(e->r_model.data(), T);
+  const size_t o_ls = o; put(e->l_src.data(), R);
+  const size_t o_ld = o; put(e->l_dst.data(), R);
+  const size_t o_it = o; put(e->items.data(), 4 * (size_t)nitems);
+  const size_t o_rd = o; put(e->red.data(), 4 * (size_t)nred);
+  HIPCHK(hipMemcpyAsync(e->meta, hb, meta_ints * 4, hipMemcpyHostToDevice, e->stream), "meta upload");
+  for (int64_t id : admitted) {
+    Request& r = e->reqs[id];
+    const size_t a = o;
+    put(r.prompt.data(), r.prompt.size());
+    HIPCHK(hipMemcpyAsync(e->tok_store + r.tok_off, hb + a, r.prompt.size() * 4, hipMemcpyHostToDevice, e->stream),
+           "prompt upload");
+    const size_t b = o;
+    put(r.blocks.data(), r.blocks.size());
+    HIPCHK(hipMemcpyAsync(e->bt_store + r.bt_off, hb + b, r.blocks.size() * 4, hipMemcpyHostToDevice, e->stream),
+           "block list upload");
+    std::vector<int32_t>().swap(r.prompt);
+  }
+  StepDev sd;
+  sd.row_tok = e->meta + o_tok;
+  sd.row_pos = e->meta + o_pos;
+  sd.row_bt = e->meta + o_bt;
+  sd.row_model = e->meta + o_mod;
+  sd.lm_src = e->meta + o_ls;
+  sd.lm_dst = e->meta + o_ld;
+  sd.items = (const AttnItem*)(e->meta + o_it);
+  sd.red = (const ReduceItem*)(e->meta + o_rd);
+
+  // ---- kernels
+  const bool bf = e->bf16;
+  const int M = (int)e->models.size();
+  const int d = g.d_model, hd = g.head_dim, nh = g.n_heads, nkv = g.n_kv_heads, F = g.ffn_dim, V = g.vocab;
+  const int qkv = (nh + 2 * nkv) * hd;
+  const size_t xn_lo = (size_t)L.Tmax * d, ao_lo = (size_t)L.Tmax * nh * hd, h_lo = (size_t)L.Tmax * F;
+  hipStream_t s = e->stream;
+  ModelPtrs mp{};
+  auto fill = [&](auto get) { for (int m = 0; m < M; ++m) mp.p[m] = get(e->models[m]); return mp; };
+
+  GemmPlanIn gin;
+  int r0 = 0;
+  for (int m = 0; m < M; ++m) {
+    if (grp_rows[m] == 0) continue;
+    gin.row0[gin.ngroups] = r0;
+    gin.nrows[gin.ngroups] = grp_rows[m];
+    gin.W[gin.ngroups] = nullptr;
+    r0 += grp_rows[m];
+    gin.ngroups++;
+  }
+  int gmodel[kMaxModels];
+  {
+    int k = 0;
+    for (int m = 0; m < M; ++m)
+      if (grp_rows[m]) gmodel[k++] = m;
+  }
+  auto weights = [&](auto get) { GemmPlanIn w = gin; for (int k = 0; k < w.ngroups; ++k) w.W[k] = get(e->models[gmodel[k]]); return w; };
+
+  if (T > 0) {
+    HIPCHK(launch_embed(s, bf, e->tok_store, sd.row_tok, sd.row_model, fill([](const ModelDev& x) { return x.embed; }),
+                        e->x, T, d), "embed");
+    int prev_split = 0;
+    size_t prev_stride = 0;
+    for (int l = 0; l < g.n_layers; ++l) {
+      GemmArgs ga;
+      int mt, nt;
+      HIPCHK(launch_add_rmsnorm(s, bf, e->x, prev_split ? e->part : nullptr, prev_split, prev_stride, nullptr,
+                                sd.row_model, T, fill([l](const ModelDev& x) { return x.attn_norm[l]; }), e->xn,
+                                xn_lo, d, g.rms_eps), "attn norm");
+      plan_gemm(e, weights([l](const ModelDev& x) { return x.wqkv[l]; }), d, qkv, EPI_F32, e->xn, xn_lo, e->part,
+                nullptr, 0, true, ga, mt, nt);
+      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "qkv gemm");
+      HIPCHK(launch_rope_kv(s, bf, e->part, ga.S, ga.out_split, sd.row_pos, sd.row_bt, e->bt_store, e->rope, e->q,
+                            e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd, T), "rope kv");
+      HIPCHK(launch_attention(s, bf, sd.items, nitems, e->q, e->kv, e->bt_store, sd.row_bt, l, e->cfg.num_kv_blocks,
+                              nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc, e->pml),
+             "attention");
+      HIPCHK(launch_attn_reduce(s, bf, sd.red, nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
+      plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), nh * hd, d, EPI_F32, e->ao, ao_lo, e->part,
+                nullptr, 0, true, ga, mt, nt);
+      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "o gemm");
+      HIPCHK(launch_add_rmsnorm(s, bf, e->x, e->part, ga.S, ga.out_split, nullptr, sd.row_model, T,
+                                fill([l](const ModelDev& x) { return x.mlp_norm[l]; }), e->xn, xn_lo, d,
+                                g.rms_eps), "mlp norm");
+      if (bf) {
+        plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), d, 2 * F, EPI_SWIGLU, e->xn, xn_lo,
+                  nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt);
+        HIPCHK(launch_gemm(s, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
+      } else {
+        plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), d, 2 * F, EPI_F32, e->xn, 0, e->part,
+                  nullptr, 0, false, ga, mt, nt);
+        HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
+        HIPCHK(launch_swiglu_f32(s, e->part, (float*)e->h, T, F), "swiglu");
+      }
+      plan_gemm(e, weights([l](const ModelDev& x) { return x.wdown[l]; }), F, d, EPI_F32, e->h, h_lo, e->part,
+                nullptr, 0, true, ga, mt, nt);
+      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "down gemm");
+      prev_split = ga.S;
+      prev_stride = ga.out_split;
+    }
+    if (R > 0) {
+      HIPCHK(launch_add_rmsnorm(s, bf, e->x, e->part, prev_split, prev_stride, sd.lm_src, sd.row_model, R,
+                                fill([](const ModelDev& x) { return x.final_norm; }), e->xn, xn_lo, d,
+                                g.rms_eps), "final norm");
+      GemmPlanIn lin;
+      int lr0 = 0;
+      for (int m = 0; m < M; ++m) {
+        if (grp_lm[m] == 0) continue;
+        lin.row0[lin.ngroups] = lr0;
+        lin.nrows[lin.ngroups] = grp_lm[m];
+        lin.W[lin.ngroups] = e->models[m].lm_head;
+        lr0 += grp_lm[m];
+        lin.ngroups++;
+      }
+      GemmArgs ga;
+      int mt, nt;
+      plan_gemm(e, lin, d, V, EPI_F32, e->xn, xn_lo, e->logits, nullptr, 0, false, ga, mt, nt);
+      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "lm head");
+      HIPCHK(launch_argmax(s, e->logits, R, V, sd.lm_dst, e->tok_store), "argmax");
+    }
+  }
+  (void)L;
+  HIPCHK(hipEventRecord(e->ev[slot], s), "event record");
+  e->ev_step[slot] = e->step_idx;
+  return MOA_OK;
+}
+
+}  // namespace
+
+moa_status moa_step(moa_engine* e, moa_step_info* info) {
+  if (!e) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (info) std::memset(info, 0, sizeof(*info));
+  if (e->pending.empty() && e->running.empty()) {
+    if (info) { info->step = -1; info->free_blocks = (int32_t)e->free_blocks.nfree; }
+    return MOA_OK;
+  }
+  const int64_t s = e->step_idx;
+  const int M = (int)e->models.size();
+  // 1 admit
+  std::vector<int64_t> admitted;
+  while (!e->pending.empty() && (int32_t)e->running.size() < e->cfg.max_num_seqs) {
+    Request& r = e->reqs[e->pending.front()];
+    if (r.need > e->free_blocks.nfree) break;
+    if (e->bt_top + r.need > e->lay.block_store) {        // block-list store full
+      if (e->running.empty()) return MOA_ENOMEM;          // nothing will free it before a collect
+      break;
+    }
+    e->free_blocks.take(r.need, r.blocks);
+    r.bt_off = e->bt_top;
+    e->bt_top += r.need;
+    r.admit_step = s;
+    r.state = 1;
+    e->running.push_back(r.id);
+    admitted.push_back(r.id);
+    e->pending.pop_front();
+  }
+  // 2 prefill, 3 decode: record per-request actions in admission order
+  struct Act { int64_t id; int kind; int start, len; };   // kind 0 prefill chunk, 1 decode
+  std::vector<Act> acts;
+  acts.reserve(e->running.size() + 8);
+  int budget = e->cfg.max_prefill_tokens;
+  int n_pre = 0, n_dec = 0;
+  for (int64_t id : e->running) {
+    if (budget <= 0) break;
+    Request& r = e->reqs[id];
+    if (r.pre < r.P) {
+      const int c = std::min(r.P - r.pre, budget);
+      acts.push_back({id, 0, r.pre, c});
+      r.chunks.push_back({s, r.pre, c});
+      r.pre += c;
+      budget -= c;
+      n_pre += c;
+      if (r.pre == r.P) { r.gen = 1; r.fresh = true; }
+    }
+  }
+  for (int64_t id : e->running) {
+    Request& r = e->reqs[id];
+    if (r.pre == r.P && !r.fresh && r.gen < r.G) {
+      acts.push_back({id, 1, r.P + r.gen - 1, 1});
+      r.gen += 1;
+      n_dec += 1;
+    }
+  }
+  // rows grouped by model: prefill chunks then decode rows, each in admission order
+  const int T = n_pre + n_dec;
+  e->r_tok.clear(); e->r_pos.clear(); e->r_bt.clear(); e->r_model.clear();
+  e->l_src.clear(); e->l_dst.clear(); e->items.clear(); e->red.clear();
+  int grp_rows[kMaxModels] = {0}, grp_lm[kMaxModels] = {0};
+  int nslots = 0;
+  std::vector<std::pair<int64_t, int>> capture_rows;   // (request, lm row)
+  for (int m = 0; m < M; ++m) {
+    for (int pass = 0; pass < 2; ++pass) {
+      for (const Act& a : acts) {
+        if (a.kind != pass) continue;
+        Request& r = e->reqs[a.id];
+        if (r.model != m) continue;
+        for (int i = 0; i < a.len; ++i) {
+          const int pos = a.start + i;
+          const int row = (int)e->r_tok.size();
+          e->r_tok.push_back((int)(r.tok_off + pos));    // prompt slot, or output gen-1 for decode
+          e->r_pos.push_back(pos);
+          e->r_bt.push_back((int)r.bt_off);
+          e->r_model.push_back(m);
+          grp_rows[m]++;
+          const int ctx = pos + 1;
+          if (a.kind == 0) {
+            e->items.push_back({row, 0, ctx, -1});
+          } else {
+            const int ns = (ctx + kSplitKeys - 1) / kSplitKeys;
+            if (ns == 1) {
+              e->items.push_back({row, 0, ctx, -1});
+            } else {
+              e->red.push_back({row, nslots, ns, 0});
+              for (int k = 0; k < ns; ++k)
+                e->items.push_back({row, k * kSplitKeys, std::min(ctx, (k + 1) * kSplitKeys), nslots + k});
+              nslots += ns;
+            }
+          }
+          const bool emits = (a.kind == 1) || (pos == r.P - 1);
+          if (emits) {
+            const int gen_idx = (a.kind == 1) ? (pos - r.P + 1) : 0;   // output index produced
+            e->l_src.push_back(row);
+            e->l_dst.push_back((int)(r.tok_off + r.P + gen_idx));
+            grp_lm[m]++;
+            if (r.capture) capture_rows.push_back({a.id, (int)e->l_src.size() - 1});
+          }
+        }
+      }
+    }
+  }
+  const int R = (int)e->l_src.size();
+  if (!e->plan_only) {
+    if (T > e->lay.Tmax || R > e->lay.Rmax || nslots > e->lay.slots_cap ||
+        (int64_t)e->items.size() > e->lay.items_cap) {
+      e->broken = true;
+      std::fprintf(stderr, "moa: step plan exceeds workspace (T=%d R=%d slots=%d)\n", T, R, nslots);
+      return MOA_EHIP;
+    }
+    moa_status st = enqueue_step(e, admitted, T, R, grp_rows, grp_lm);
+    if (st != MOA_OK) return st;
+    for (auto& cr : capture_rows) {
+      Request& r = e->reqs[cr.first];
+      const int row = cr.second;
+      const int gen_idx = e->l_dst[row] - (int)(r.tok_off + r.P);
+      hipError_t err = hipMemcpyAsync(r.capture + (size_t)gen_idx * e->cfg.model.vocab,
+                                      e->logits + (size_t)row * e->cfg.model.vocab,
+                                      (size_t)e->cfg.model.vocab * 4, hipMemcpyDeviceToHost, e->stream);
+      if (err != hipSuccess) return hip_fail(e, err, "logit capture");
+    }
+  } else {
+    for (int64_t id : admitted) std::vector<int32_t>().swap(e->reqs[id].prompt);
+  }
+  // 4 retire
+  int n_ret = 0;
+  std::vector<int64_t> keep;
+  keep.reserve(e->running.size());
+  for (int64_t id : e->running) {
+    Request& r = e->reqs[id];
+    if (r.gen == r.G) {
+      e->free_blocks.give(r.blocks);
+      r.finish_step = s;
+      r.state = 2;
+      e->done.push_back(id);
+      n_ret++;
+    } else {
+      keep.push_back(id);
+    }
+    r.fresh = false;
+  }
+  e->running.swap(keep);
+  e->trace.push_back({s, (int64_t)admitted.size(), n_pre, n_dec, n_ret, e->free_blocks.nfree});
+  e->step_idx++;
+  if (info) {
+    info->step = s;
+    info->admitted = (int32_t)admitted.size();
+    info->prefill_tokens = n_pre;
+    info->decode_rows = n_dec;
+    info->finished = n_ret;
+    info->running = (int32_t)e->running.size();
+    info->pending = (int32_t)e->pending.size();
+    info->free_blocks = (int32_t)e->free_blocks.nfree;
+  }
+  return MOA_OK;
+}
+
+moa_status moa_collect(moa_engine* e, int64_t upto_step, moa_result* res, int32_t cap, int32_t* n_out,
+                       int32_t* tok_buf, int64_t tok_cap) {
+  if (!e || !n_out) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (upto_step < 0) upto_step = e->step_idx - 1;
+  int32_t n = 0;
+  int64_t ntok = 0, last = -1;
+  for (int64_t id : e->done) {
+    const Request& r = e->reqs[id];
+    if (r.finish_step > upto_step) break;          // done is ordered by finish step
+    n++;
+    ntok += r.G;
+    last = std::max(last, r.finish_step);
+  }
+  *n_out = n;
+  if (n == 0) return MOA_OK;
+  if (!res || !tok_buf || n > cap || ntok > tok_cap) return MOA_EINVAL;
+  if (!e->plan_only) {
+    // Wait for the last step that retired one of them (if its staging slot has
+    // been reused since, that step already completed), then copy on the side stream.
+    for (int i = 0; i < kStageSlots; ++i)
+      if (e->ev_step[i] == last) HIPCHK(hipEventSynchronize(e->ev[i]), "collect wait");
+    if ((size_t)ntok > e->pinned_out_cap) {
+      if (e->pinned_out) HIPCHK(hipHostFree(e->pinned_out), "hipHostFree");
+      e->pinned_out = nullptr;
+      size_t cap2 = std::max((size_t)ntok, (size_t)1 << 16);
+      HIPCHK(hipHostMalloc((void**)&e->pinned_out, cap2 * 4, hipHostMallocDefault), "hipHostMalloc");
+      e->pinned_out_cap = cap2;
+    }
+    int64_t o = 0;
+    for (int32_t i = 0; i < n; ++i) {
+      const Request& r = e->reqs[e->done[i]];
+      HIPCHK(hipMemcpyAsync(e->pinned_out + o, e->tok_store + r.tok_off + r.P, (size_t)r.G * 4,
+                            hipMemcpyDeviceToHost, e->copy_stream), "collect copy");
+      o += r.G;
+    }
+    HIPCHK(hipStreamSynchronize(e->copy_stream), "collect sync");
+    std::memcpy(tok_buf, e->pinned_out, (size_t)ntok * 4);
+  } else {
+    for (int64_t i = 0; i < ntok; ++i) tok_buf[i] = -1;
+  }
+  int64_t o = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    Request& r = e->reqs[e->done[i]];
+    res[i].request_id = r.id;
+    res[i].model_id = r.model;
+    res[i].n_tokens = r.G;
+    res[i].tok_offset = o;
+    res[i].finish_step = r.finish_step;
+    o += r.G;
+    r.state = 3;
+    r.capture = nullptr;
+    e->live -= 1;
+  }
+  e->done.erase(e->done.begin(), e->done.begin() + n);
+  return MOA_OK;
+}
+
+moa_status moa_sync(moa_engine* e) {
+  if (!e) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (!e->plan_only) HIPCHK(hipStreamSynchronize(e->stream), "sync");
+  return MOA_OK;
+}
+
+moa_status moa_debug_request(moa_engine* e, int64_t id, moa_request_info* info) {
+  if (!e || !info || id < 0 || id >= (int64_t)e->reqs.size()) return MOA_EINVAL;
+  const Request& r = e->reqs[id];
+  info->model_id = r.model;
+  info->prompt_len = r.P;
+  info->max_new_tokens = r.G;
+  info->n_blocks = (int32_t)r.blocks.size();
+  info->admit_step = r.admit_step;
+  info->finish_step = r.finish_step;
+  info->n_chunks = (int32_t)r.chunks.size();
+  info->state = r.state;
+  return MOA_OK;
+}
+
+moa_status moa_debug_block_table(moa_engine* e, int64_t id, int32_t* out, int32_t cap, int32_t* n_out) {
+  if (!e || !n_out || id < 0 || id >= (int64_t)e->reqs.size()) return MOA_EINVAL;
+  const Request& r = e->reqs[id];
+  *n_out = (int32_t)r.blocks.size();
+  if ((int32_t)r.blocks.size() > cap || (!out && !r.blocks.empty())) return MOA_EINVAL;
+  if (!r.blocks.empty()) std::memcpy(out, r.blocks.data(), r.blocks.size() * 4);
+  return MOA_OK;
+}
+
+moa_status moa_debug_chunks(moa_engine* e, int64_t id, int64_t* out, int32_t cap, int32_t* n_out) {
+  if (!e || !n_out || id < 0 || id >= (int64_t)e->reqs.size()) return MOA_EINVAL;
+  const Request& r = e->reqs[id];
+  *n_out = (int32_t)r.chunks.size();
+  if ((int32_t)r.chunks.size() > cap || (!out && !r.chunks.empty())) return MOA_EINVAL;
+  for (size_t i = 0; i < r.chunks.size(); ++i)
+    for (int k = 0; k < 3; ++k) out[3 * i + k] = r.chunks[i][k];
+  return MOA_OK;
+}
+
+moa_status moa_debug_steps(moa_engine* e, int64_t* out, int64_t cap, int64_t* n_out) {
+  if (!e || !n_out) return MOA_EINVAL;
+  *n_out = (int64_t)e->trace.size();
+  if ((int64_t)e->trace.size() > cap || (!out && !e->trace.empty())) return MOA_EINVAL;
+  for (size_t i = 0; i < e->trace.size(); ++i)
+    for (int k = 0; k < 6; ++k) out[6 * i + k] = e->trace[i][k];
+  return MOA_OK;
+}
+
+moa_status moa_debug_capture_logits(moa_engine* e, int64_t id, float* host_logits) {
+  if (!e || !host_logits || id < 0 || id >= (int64_t)e->reqs.size()) return MOA_EINVAL;
+  Request& r = e->reqs[id];
+  if (r.state >= 2 || (r.pre == r.P && r.gen > 0)) return MOA_ESTATE;
+  r.capture = host_logits;
+  return MOA_OK;
+}
+
+}  // extern "C"

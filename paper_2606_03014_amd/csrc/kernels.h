@@ -1,0 +1,88 @@
+// Internal launch interface between the engine's host code and its gfx950
+// kernels. Not part of the C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+#include <cstddef>
+
+namespace moa {
+
+constexpr int kMaxModels = 8;     // models per engine (grouped launches carry one slot each)
+constexpr int kBlock = 16;        // KV slots per block
+constexpr int kSplitKeys = 256;   // keys per decode-attention split (fixed: results do not depend on the batch)
+
+struct ModelPtrs { const void* p[kMaxModels]; };
+
+// One contiguous segment of rows that shares a weight matrix.
+struct GemmGroup {
+  const void* W;    // bf16: tile-shuffled [N/16][K/32][64 lanes][8]; f32: row-major [N][K]
+  int row0, nrows;  // rows [row0, row0 + nrows) of X and of the output
+  int n_mc;         // row chunks of 16*MT rows
+  int item0;        // first wave item of this group
+};
+
+constexpr int kMaxGroups = kMaxModels;
+
+struct GemmArgs {
+  GemmGroup g[kMaxGroups];
+  int ngroups;
+  int total_items;
+  const void* X;       // [rows][K] activations, row stride K: f32, or the hi plane of a split-bf16 pair
+  size_t x_lo;         // bf16: elements from the hi plane to the lo plane (x ~= hi + lo)
+  int K, N;
+  int S;               // k splits (partial sums out[s])
+  int ksteps;          // 32-wide k steps per split
+  float* out;          // f32 output / partials: out + s*out_split + row*N + n
+  size_t out_split;
+  uint16_t* hout;      // SwiGLU epilogue output, split bf16 [rows][N/2] (hi), lo plane at +h_lo
+  size_t h_lo;
+};
+
+enum Epilogue { EPI_F32 = 0, EPI_SWIGLU = 1 };
+
+// Attention work item: one query row against keys [k0, k1) of its request.
+struct AttnItem { int row, k0, k1, slot; };   // slot < 0: write the final output
+struct ReduceItem { int row, slot0, nslots, pad; };
+
+struct StepDev {
+  const int* row_tok;    // [T] index into the token store
+  const int* row_pos;    // [T]
+  const int* row_bt;     // [T] offset of the row's block list in the block store
+  const int* row_model;  // [T]
+  const int* lm_src;     // [R] row that produces a token
+  const int* lm_dst;     // [R] token-store slot the token goes to
+  const AttnItem* items; // attention items
+  const ReduceItem* red; // split-combine items
+};
+
+// All launchers enqueue on `st` and return hipGetLastError().
+hipError_t launch_embed(hipStream_t st, bool bf16, const int* tok_store, const int* row_tok,
+                        const int* row_model, ModelPtrs embed, float* x, int T, int d);
+
+// bf16 mode writes split-bf16 output: hi at out, lo at out + out_lo (elements).
+hipError_t launch_add_rmsnorm(hipStream_t st, bool bf16, float* x, const float* part, int nsplit,
+                              size_t split_stride, const int* gather, const int* row_model, int nrows,
+                              ModelPtrs gamma, void* out, size_t out_lo, int d, float eps);
+
+hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt);
+
+hipError_t launch_swiglu_f32(hipStream_t st, const float* gu, float* h, int T, int ffn);
+
+hipError_t launch_rope_kv(hipStream_t st, bool bf16, const float* part, int nsplit, size_t split_stride,
+                          const int* row_pos, const int* row_bt, const int* bt_store,
+                          const float2* rope_tab, float* q, void* kv, int layer, int num_blocks,
+                          int n_h, int n_kv, int hd, int T);
+
+hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, int nitems,
+                            const float* q, const void* kv, const int* bt_store, const int* row_bt,
+                            int layer, int num_blocks, int n_h, int n_kv, int hd, float scale,
+                            void* out, size_t out_lo, float* pacc, float* pml);
+
+hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, int nred,
+                              const float* pacc, const float* pml, void* out, size_t out_lo, int n_h,
+                              int hd);
+
+hipError_t launch_argmax(hipStream_t st, const float* logits, int R, int V, const int* lm_dst,
+                         int* tok_store);
+
+}  // namespace moa

@@ -1,0 +1,646 @@
+// gfx950 (CDNA4) kernels of the ragged MoA generation step.
+//
+// One engine step runs every co-resident model's rows as one ragged batch:
+// rows of the same model are contiguous, and each kernel class is launched
+// once per layer for all models (grouped over models), so the weights of each
+// active model stream from HBM once per step. The kernels are written for
+// 64-wide wavefronts; the dense contractions use the bf16 MFMA
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
+#include "kernels.h"
+
+#include <hip/hip_runtime.h>
+#include <climits>
+#include <cmath>
+
+namespace moa {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// Split-bf16 store: v ~= hi + lo with hi = bf16(v), lo = bf16(v - hi); the
+// pair carries ~16 significant bits, so a GEMM fed hi and lo (two MFMAs per
+// weight fragment) sees the fp32 activation almost exactly while the weights
+// stay bf16.
+__device__ __forceinline__ void store_split(uint16_t* p, size_t lo, size_t i, float v) {
+  const uint16_t h = f2bf(v);
+  p[i] = h;
+  p[i + lo] = f2bf(v - bf2f(h));
+}
+
+__device__ __forceinline__ const void* pick(const ModelPtrs& mp, int m) {
+  const void* r = mp.p[0];
+#pragma unroll
+  for (int i = 1; i < kMaxModels; ++i)
+    if (i == m) r = mp.p[i];
+  return r;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// Sum over a 256-thread block; every thread gets the result.
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float t = red[0] + red[1] + red[2] + red[3];
+  __syncthreads();
+  return t;
+}
+
+// ---------------------------------------------------------------- embedding
+// x[t] = E_model[tok] in fp32 (the residual stream is fp32 in every mode).
+template <bool BF>
+__global__ __launch_bounds__(256) void k_embed(const int* __restrict__ tok_store,
+                                               const int* __restrict__ row_tok,
+                                               const int* __restrict__ row_model, ModelPtrs embed,
+                                               float* __restrict__ x, int d) {
+  const int t = blockIdx.x;
+  const int tok = tok_store[row_tok[t]];
+  const void* E = pick(embed, row_model[t]);
+  float* xr = x + (size_t)t * d;
+  if (BF) {
+    const uint16_t* e = (const uint16_t*)E + (size_t)tok * d;
+    for (int i = threadIdx.x; i < d; i += 256) xr[i] = bf2f(e[i]);
+  } else {
+    const float* e = (const float*)E + (size_t)tok * d;
+    for (int i = threadIdx.x; i < d; i += 256) xr[i] = e[i];
+  }
+}
+
+// ------------------------------------------------- residual add + RMSNorm
+// x[r] += sum_s part[s][r] (split-K partial sums of the previous projection),
+// out[j] = x[r] * rsqrt(mean(x[r]^2) + eps) * gamma, r = gather ? gather[j] : j.
+template <bool BF>
+__global__ __launch_bounds__(256) void k_add_rmsnorm(float* __restrict__ x, const float* __restrict__ part,
+                                                     int nsplit, size_t split_stride,
+                                                     const int* __restrict__ gather,
+                                                     const int* __restrict__ row_model, ModelPtrs gamma,
+                                                     void* __restrict__ out, size_t out_lo, int d, float eps) {
+  __shared__ float red[4];
+  const int j = blockIdx.x;
+  const int r = gather ? gather[j] : j;
+  float* xr = x + (size_t)r * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float v = xr[i];
+    for (int s = 0; s < nsplit; ++s) v += part[(size_t)s * split_stride + (size_t)r * d + i];
+    if (nsplit) xr[i] = v;
+    ss += v * v;
+  }
+  ss = block_sum256(ss, red);
+  const float scale = rsqrtf(ss / (float)d + eps);
+  const void* g = pick(gamma, row_model[r]);
+  if (BF) {
+    uint16_t* o = (uint16_t*)out + (size_t)j * d;
+    const uint16_t* gg = (const uint16_t*)g;
+    for (int i = threadIdx.x; i < d; i += 256) store_split(o, out_lo, i, xr[i] * scale * bf2f(gg[i]));
+  } else {
+    float* o = (float*)out + (size_t)j * d;
+    const float* gg = (const float*)g;
+    for (int i = threadIdx.x; i < d; i += 256) o[i] = xr[i] * scale * gg[i];
+  }
+}
+
+// ------------------------------------------------------------ bf16 GEMM
+// Y = X . W^T for every group (model) of rows, on MFMA 16x16x32 bf16.
+//
+// Work unit = one wavefront: a chunk of 16*MT rows x NT tiles of 16 output
+// columns x one k-split. Weights are stored tile-shuffled so that one MFMA
+// B-fragment (16 columns x 32 k) is 1 KB contiguous, lane-ordered: a wave's
+// weight read is a single fully coalesced 1 KB burst per fragment, and a
+// 16-column tile streams K*32 bytes contiguously. Waves of one workgroup
+// cover consecutive row chunks of the same columns, so a weight fragment
+// reaches HBM once and the other waves hit the cache.
+//
+// MFMA operand layout used here (lane l of 64): A = rows l%16, k = 8*(l/16)..+8;
+// B = column l%16, same k; D = column l%16, rows 4*(l/16)..+4.
+template <int MT, int NT, int EPI, int U>
+__global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (item >= a.total_items) return;
+  const void* Wg = a.g[0].W;
+  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroups; ++i) {
+    if (i < a.ngroups && a.g[i].item0 <= item) {
+      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
+    }
+  }
+  const int idx = item - item0;
+  const int mc = idx % n_mc;
+  const int rest = idx / n_mc;
+  const int s = rest % a.S;
+  const int nb = rest / a.S;
+  const int ks0 = s * a.ksteps;
+  const int nt0 = nb * NT;
+  const int KS = a.K >> 5;
+
+  const uint4* W = (const uint4*)Wg;
+  const uint4* wp[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) wp[j] = W + ((size_t)(nt0 + j) * KS + ks0) * 64 + lane;
+
+  const int rbase = row0 + mc * MT * 16;
+  const int rend = row0 + nrows;
+  const uint16_t* X = (const uint16_t*)a.X;
+  const uint4* xp[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) {
+    int r = min(rbase + m * 16 + (lane & 15), rend - 1);
+    xp[m] = (const uint4*)(X + (size_t)r * a.K + ks0 * 32 + (lane >> 4) * 8);
+  }
+  const size_t xlo = a.x_lo / 8;     // hi -> lo plane distance in uint4 units
+
+  f32x4_t acc[MT][NT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[m][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int kk = 0; kk < a.ksteps; kk += U) {
+    uint4 b[U][NT], xa[U][MT], xl[U][MT];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) b[u][j] = wp[j][(kk + u) * 64];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        xa[u][m] = xp[m][(kk + u) * 4];
+        xl[u][m] = xp[m][(kk + u) * 4 + xlo];
+      }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xa[u][m]),
+                                                              __builtin_bit_cast(bf16x8_t, b[u][j]),
+                                                              acc[m][j], 0, 0, 0);
+          acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xl[u][m]),
+                                                              __builtin_bit_cast(bf16x8_t, b[u][j]),
+                                                              acc[m][j], 0, 0, 0);
+        }
+  }
+
+  const int col = lane & 15;
+  const int rq = (lane >> 4) * 4;
+  if (EPI == EPI_F32) {
+    float* out = a.out + (size_t)s * a.out_split;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = rbase + m * 16 + rq + i;
+          if (r < rend) out[(size_t)r * a.N + (nt0 + j) * 16 + col] = acc[m][j][i];
+        }
+  } else {
+    // tiles (2p, 2p+1) are (gate, up) of the same 16 hidden units
+    const int half = a.N >> 1;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+      for (int p = 0; p < NT / 2; ++p)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = rbase + m * 16 + rq + i;
+          if (r < rend) {
+            const float g = acc[m][2 * p][i], u = acc[m][2 * p + 1][i];
+            const float hv = g / (1.f + __expf(-g)) * u;
+            store_split(a.hout, a.h_lo, (size_t)r * half + ((nt0 >> 1) + p) * 16 + col, hv);
+          }
+        }
+  }
+}
+
+// ------------------------------------------------------------ fp32 GEMM
+// Plain fp32 FMA GEMM for the fp32 engine mode: a workgroup computes 16 rows
+// x 64 columns; W is row-major [N][K].
+__global__ __launch_bounds__(256) void k_gemm_f32(GemmArgs a) {
+  const int item = blockIdx.x;
+  const void* Wg = a.g[0].W;
+  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroups; ++i) {
+    if (i < a.ngroups && a.g[i].item0 <= item) {
+      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
+    }
+  }
+  const int idx = item - item0;
+  const int mc = idx % n_mc, nb = idx / n_mc;
+  const int colw = nb * 64 + (threadIdx.x & 63);
+  const int rb = row0 + mc * 16 + (threadIdx.x >> 6) * 4;
+  const int rend = row0 + nrows;
+  const float* W = (const float*)Wg + (size_t)colw * a.K;
+  const float* X = (const float*)a.X;
+  const float* xr[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) xr[i] = X + (size_t)min(rb + i, rend - 1) * a.K;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < a.K; ++k) {
+    const float w = W[k];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc[i] = fmaf(xr[i][k], w, acc[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    if (rb + i < rend) a.out[(size_t)(rb + i) * a.N + colw] = acc[i];
+}
+
+// h = silu(gate) * up for the fp32 mode; gu rows are [gate(ffn) | up(ffn)].
+__global__ __launch_bounds__(256) void k_swiglu_f32(const float* __restrict__ gu, float* __restrict__ h,
+                                                    int ffn) {
+  const int t = blockIdx.x;
+  const float* r = gu + (size_t)t * 2 * ffn;
+  for (int i = threadIdx.x; i < ffn; i += 256) {
+    const float g = r[i];
+    h[(size_t)t * ffn + i] = g / (1.f + expf(-g)) * r[ffn + i];
+  }
+}
+
+// ------------------------------------------------------ RoPE + KV append
+// Reduces the QKV partial sums, rotates q and k (pairs (i, i + hd/2) turned by
+// pos * theta^(-2i/hd), table precomputed in fp64 and rounded to fp32), stores
+// q (fp32), and writes k, v (rounded to the cache type) into the row's paged-KV slot: block bt[pos / 16], slot
+// pos % 16. Pool layout: [layer][block][kv_head][K|V][16][hd].
+template <bool BF>
+__global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ part, int nsplit, size_t split_stride,
+                                                 const int* __restrict__ row_pos, const int* __restrict__ row_bt,
+                                                 const int* __restrict__ bt_store, const float2* __restrict__ tab,
+                                                 float* __restrict__ qv, void* __restrict__ kvv, int layer, int NB,
+                                                 int n_h, int n_kv, int hd) {
+  const int t = blockIdx.x;
+  const int pos = row_pos[t];
+  const int half = hd >> 1;
+  const int qkv = (n_h + 2 * n_kv) * hd;
+  const float* pr = part + (size_t)t * qkv;
+  const int blk = bt_store[row_bt[t] + (pos >> 4)];
+  const int off = pos & 15;
+  const size_t hs = (size_t)2 * kBlock * hd;
+  const size_t lbase = ((size_t)layer * NB + blk) * n_kv * hs;
+  for (int i = threadIdx.x; i < (n_h + n_kv) * half; i += 256) {
+    const int head = i / half, jj = i - head * half;
+    const int c = head * hd + jj;
+    float x1 = 0.f, x2 = 0.f;
+    for (int s = 0; s < nsplit; ++s) {
+      x1 += pr[(size_t)s * split_stride + c];
+      x2 += pr[(size_t)s * split_stride + c + half];
+    }
+    const float2 cs = tab[(size_t)pos * half + jj];
+    const float y1 = x1 * cs.x - x2 * cs.y;
+    const float y2 = x2 * cs.x + x1 * cs.y;
+    if (head < n_h) {
+      const size_t o = ((size_t)t * n_h + head) * hd + jj;
+      qv[o] = y1;
+      qv[o + half] = y2;
+    } else {
+      const size_t o = lbase + (size_t)(head - n_h) * hs + off * hd + jj;
+      if (BF) { ((uint16_t*)kvv)[o] = f2bf(y1); ((uint16_t*)kvv)[o + half] = f2bf(y2); }
+      else { ((float*)kvv)[o] = y1; ((float*)kvv)[o + half] = y2; }
+    }
+  }
+  for (int i = threadIdx.x; i < n_kv * hd; i += 256) {
+    const int kh = i / hd, dd = i - kh * hd;
+    const int c = (n_h + n_kv) * hd + i;
+    float v = 0.f;
+    for (int s = 0; s < nsplit; ++s) v += pr[(size_t)s * split_stride + c];
+    const size_t o = lbase + (size_t)kh * hs + kBlock * hd + off * hd + dd;
+    if (BF) ((uint16_t*)kvv)[o] = f2bf(v);
+    else ((float*)kvv)[o] = v;
+  }
+}
+
+// ------------------------------------------------ paged attention (split-KV)
+// One workgroup = one query row x one KV head x one key range [k0, k1); its
+// GQ wavefronts are the GQ query heads that share the KV head, so each K/V
+// tile is read from HBM once for the whole group. Tiles of 64 keys are
+// staged in LDS with 16-byte coalesced loads (a 16-slot block of one KV head
+// is contiguous). In a tile, lane l owns key 8*p + l/8 (p = 0..7) and head-dim
+// chunk l%8: q.k partial dots are combined across the 8 lanes of a key with
+// xor-shuffles, the tile max across the wavefront with shuffles, and P.V
+// accumulates per lane on its own keys and dims (combined once at the end).
+// Softmax runs in base 2 on scores pre-scaled by log2(e)/sqrt(hd).
+template <int HD, int GQ, bool BF>
+__global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ items, const float* __restrict__ qv,
+                                                  const void* __restrict__ kvv, const int* __restrict__ bt_store,
+                                                  const int* __restrict__ row_bt, int layer, int NB, int n_h,
+                                                  int n_kv, float scale_log2, void* __restrict__ outv,
+                                                  size_t out_lo, float* __restrict__ pacc, float* __restrict__ pml) {
+  constexpr int TK = 64;
+  constexpr int CH = HD / 8;
+  constexpr int ESZ = BF ? 2 : 4;
+  constexpr int ROWB = HD * ESZ;
+  constexpr int CPR = ROWB / 16;
+  constexpr int NCH = 2 * TK * CPR;
+  __shared__ __align__(16) unsigned char sK[TK * ROWB];
+  __shared__ __align__(16) unsigned char sV[TK * ROWB];
+
+  const AttnItem it = items[blockIdx.x];
+  const int kvh = blockIdx.y;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int g8 = lane >> 3, c8 = lane & 7;
+  const int h = kvh * GQ + w;
+
+  float q[CH];
+  {
+    const size_t qo = ((size_t)it.row * n_h + h) * HD + c8 * CH;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) q[i] = qv[qo + i];
+  }
+  float m = -INFINITY, l = 0.f, acc[CH];
+#pragma unroll
+  for (int i = 0; i < CH; ++i) acc[i] = 0.f;
+
+  const int* bt = bt_store + row_bt[it.row];
+  const size_t hs = (size_t)2 * kBlock * HD;          // elements per (block, kv head)
+  const unsigned char* pool = (const unsigned char*)kvv;
+  const size_t layer_base = (size_t)layer * NB;
+
+  for (int t0 = it.k0; t0 < it.k1; t0 += TK) {
+    for (int c = threadIdx.x; c < NCH; c += GQ * 64) {
+      const int isV = c / (TK * CPR);
+      const int rem = c - isV * (TK * CPR);
+      const int key = rem / CPR, cc = rem - key * CPR;
+      const int p = t0 + key;
+      uint4 val = make_uint4(0u, 0u, 0u, 0u);
+      if (p < it.k1) {
+        const int blk = bt[p >> 4];
+        const size_t e = ((layer_base + blk) * n_kv + kvh) * hs + (size_t)isV * kBlock * HD + (size_t)(p & 15) * HD;
+        val = *(const uint4*)(pool + e * ESZ + cc * 16);
+      }
+      *(uint4*)((isV ? sV : sK) + key * ROWB + cc * 16) = val;
+    }
+    __syncthreads();
+
+    float s[8];
+#pragma unroll
+    for (int p8 = 0; p8 < 8; ++p8) {
+      const int key = p8 * 8 + g8;
+      float dot = 0.f;
+      if (BF) {
+        const uint16_t* kr = (const uint16_t*)(sK + key * ROWB) + c8 * CH;
+#pragma unroll
+        for (int i = 0; i < CH; ++i) dot = fmaf(q[i], bf2f(kr[i]), dot);
+      } else {
+        const float* kr = (const float*)(sK + key * ROWB) + c8 * CH;
+#pragma unroll
+        for (int i = 0; i < CH; ++i) dot = fmaf(q[i], kr[i], dot);
+      }
+      dot += __shfl_xor(dot, 1, 64);
+      dot += __shfl_xor(dot, 2, 64);
+      dot += __shfl_xor(dot, 4, 64);
+      s[p8] = (t0 + key < it.k1) ? dot * scale_log2 : -INFINITY;
+    }
+    float mx = s[0];
+#pragma unroll
+    for (int p8 = 1; p8 < 8; ++p8) mx = fmaxf(mx, s[p8]);
+    mx = fmaxf(mx, __shfl_xor(mx, 8, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mnew = fmaxf(m, mx);
+    const float alpha = exp2f(m - mnew);
+    l *= alpha;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) acc[i] *= alpha;
+#pragma unroll
+    for (int p8 = 0; p8 < 8; ++p8) {
+      const float pj = exp2f(s[p8] - mnew);
+      l += pj;
+      const int key = p8 * 8 + g8;
+      if (BF) {
+        const uint16_t* vr = (const uint16_t*)(sV + key * ROWB) + c8 * CH;
+#pragma unroll
+        for (int i = 0; i < CH; ++i) acc[i] = fmaf(pj, bf2f(vr[i]), acc[i]);
+      } else {
+        const float* vr = (const float*)(sV + key * ROWB) + c8 * CH;
+#pragma unroll
+        for (int i = 0; i < CH; ++i) acc[i] = fmaf(pj, vr[i], acc[i]);
+      }
+    }
+    m = mnew;
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    acc[i] += __shfl_xor(acc[i], 8, 64);
+    acc[i] += __shfl_xor(acc[i], 16, 64);
+    acc[i] += __shfl_xor(acc[i], 32, 64);
+  }
+  l += __shfl_xor(l, 8, 64);
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (g8 == 0) {
+    if (it.slot < 0) {
+      const float inv = 1.f / l;
+      const size_t o = ((size_t)it.row * n_h + h) * HD + c8 * CH;
+#pragma unroll
+      for (int i = 0; i < CH; ++i) {
+        if (BF) store_split((uint16_t*)outv, out_lo, o + i, acc[i] * inv);
+        else ((float*)outv)[o + i] = acc[i] * inv;
+      }
+    } else {
+      const size_t o = ((size_t)it.slot * n_h + h) * HD + c8 * CH;
+#pragma unroll
+      for (int i = 0; i < CH; ++i) pacc[o + i] = acc[i];
+      if (c8 == 0) {
+        pml[((size_t)it.slot * n_h + h) * 2] = m;
+        pml[((size_t)it.slot * n_h + h) * 2 + 1] = l;
+      }
+    }
+  }
+}
+
+// Combine the key-range partials of one row (fixed order over ranges).
+template <bool BF>
+__global__ void k_attn_reduce(const ReduceItem* __restrict__ red, const float* __restrict__ pacc,
+                              const float* __restrict__ pml, void* __restrict__ outv, size_t out_lo, int n_h,
+                              int hd) {
+  const ReduceItem it = red[blockIdx.x];
+  const int h = blockIdx.y;
+  const int dd = threadIdx.x;
+  float M = -INFINITY;
+  for (int s = 0; s < it.nslots; ++s) M = fmaxf(M, pml[((size_t)(it.slot0 + s) * n_h + h) * 2]);
+  float L = 0.f, o = 0.f;
+  for (int s = 0; s < it.nslots; ++s) {
+    const size_t b = (size_t)(it.slot0 + s) * n_h + h;
+    const float wgt = exp2f(pml[b * 2] - M);
+    L += pml[b * 2 + 1] * wgt;
+    o += pacc[b * hd + dd] * wgt;
+  }
+  const size_t oo = ((size_t)it.row * n_h + h) * hd + dd;
+  if (BF) store_split((uint16_t*)outv, out_lo, oo, o / L);
+  else ((float*)outv)[oo] = o / L;
+}
+
+// ------------------------------------------------------------------ argmax
+// Greedy sampler: the largest fp32 logit, ties to the lowest token id; the
+// token is written into the device token store (it feeds the next step).
+__global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits, int V,
+                                                const int* __restrict__ lm_dst, int* __restrict__ tok) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  const int r = blockIdx.x;
+  const float* lr = logits + (size_t)r * V;
+  float best = -INFINITY;
+  int bi = INT_MAX;
+  for (int v = threadIdx.x; v < V; v += 256) {
+    const float x = lr[v];
+    if (x > best) { best = x; bi = v; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bi, o, 64);
+    if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { sv[w] = best; si[w] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    best = sv[0];
+    bi = si[0];
+    for (int k = 1; k < 4; ++k)
+      if (sv[k] > best || (sv[k] == best && si[k] < bi)) { best = sv[k]; bi = si[k]; }
+    tok[lm_dst[r]] = (bi == INT_MAX) ? 0 : bi;
+  }
+}
+
+// =============================================================== launchers
+
+hipError_t launch_embed(hipStream_t st, bool bf16, const int* tok_store, const int* row_tok,
+                        const int* row_model, ModelPtrs embed, float* x, int T, int d) {
+  if (T <= 0) return hipSuccess;
+  if (bf16) k_embed<true><<<T, 256, 0, st>>>(tok_store, row_tok, row_model, embed, x, d);
+  else k_embed<false><<<T, 256, 0, st>>>(tok_store, row_tok, row_model, embed, x, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_add_rmsnorm(hipStream_t st, bool bf16, float* x, const float* part, int nsplit,
+                              size_t split_stride, const int* gather, const int* row_model, int nrows,
+                              ModelPtrs gamma, void* out, size_t out_lo, int d, float eps) {
+  if (nrows <= 0) return hipSuccess;
+  if (bf16)
+    k_add_rmsnorm<true><<<nrows, 256, 0, st>>>(x, part, nsplit, split_stride, gather, row_model, gamma, out, out_lo,
+                                               d, eps);
+  else
+    k_add_rmsnorm<false><<<nrows, 256, 0, st>>>(x, part, nsplit, split_stride, gather, row_model, gamma, out, out_lo,
+                                                d, eps);
+  return hipGetLastError();
+}
+
+template <int MT, int NT, int EPI>
+static void gemm_u(hipStream_t st, const GemmArgs& a, int blocks) {
+  if (a.ksteps % 8 == 0) k_gemm_bf16<MT, NT, EPI, 8><<<blocks, 256, 0, st>>>(a);
+  else k_gemm_bf16<MT, NT, EPI, 4><<<blocks, 256, 0, st>>>(a);
+}
+
+template <int MT>
+static void gemm_nt(hipStream_t st, const GemmArgs& a, int blocks, int epi, int nt) {
+  if (epi == EPI_SWIGLU) gemm_u<MT, 2, EPI_SWIGLU>(st, a, blocks);
+  else if (nt == 2) gemm_u<MT, 2, EPI_F32>(st, a, blocks);
+  else gemm_u<MT, 1, EPI_F32>(st, a, blocks);
+}
+
+hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt) {
+  if (a.total_items <= 0) return hipSuccess;
+  if (!bf16) {
+    k_gemm_f32<<<a.total_items, 256, 0, st>>>(a);
+    return hipGetLastError();
+  }
+  const int blocks = (a.total_items + 3) / 4;
+  if (mt == 1) gemm_nt<1>(st, a, blocks, epi, nt);
+  else if (mt == 2) gemm_nt<2>(st, a, blocks, epi, nt);
+  else gemm_nt<4>(st, a, blocks, epi, nt);
+  return hipGetLastError();
+}
+
+hipError_t launch_swiglu_f32(hipStream_t st, const float* gu, float* h, int T, int ffn) {
+  if (T <= 0) return hipSuccess;
+  k_swiglu_f32<<<T, 256, 0, st>>>(gu, h, ffn);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope_kv(hipStream_t st, bool bf16, const float* part, int nsplit, size_t split_stride,
+                          const int* row_pos, const int* row_bt, const int* bt_store,
+                          const float2* rope_tab, float* q, void* kv, int layer, int num_blocks,
+                          int n_h, int n_kv, int hd, int T) {
+  if (T <= 0) return hipSuccess;
+  if (bf16)
+    k_rope_kv<true><<<T, 256, 0, st>>>(part, nsplit, split_stride, row_pos, row_bt, bt_store, rope_tab, q, kv,
+                                       layer, num_blocks, n_h, n_kv, hd);
+  else
+    k_rope_kv<false><<<T, 256, 0, st>>>(part, nsplit, split_stride, row_pos, row_bt, bt_store, rope_tab, q, kv,
+                                        layer, num_blocks, n_h, n_kv, hd);
+  return hipGetLastError();
+}
+
+template <int HD, bool BF>
+static hipError_t attn_gq(hipStream_t st, int gq, dim3 grid, const AttnItem* items, const float* q, const void* kv,
+                          const int* bt, const int* row_bt, int layer, int NB, int n_h, int n_kv, float sl2,
+                          void* out, size_t out_lo, float* pacc, float* pml) {
+  switch (gq) {
+    case 1: k_attn<HD, 1, BF><<<grid, 64, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 2: k_attn<HD, 2, BF><<<grid, 128, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 4: k_attn<HD, 4, BF><<<grid, 256, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 8: k_attn<HD, 8, BF><<<grid, 512, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, int nitems,
+                            const float* q, const void* kv, const int* bt_store, const int* row_bt,
+                            int layer, int num_blocks, int n_h, int n_kv, int hd, float scale,
+                            void* out, size_t out_lo, float* pacc, float* pml) {
+  if (nitems <= 0) return hipSuccess;
+  const int gq = n_h / n_kv;
+  const float sl2 = scale * 1.4426950408889634f;
+  dim3 grid(nitems, n_kv);
+  if (hd == 64) {
+    return bf16 ? attn_gq<64, true>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml)
+                : attn_gq<64, false>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
+  }
+  if (hd == 128) {
+    return bf16 ? attn_gq<128, true>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml)
+                : attn_gq<128, false>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, int nred,
+                              const float* pacc, const float* pml, void* out, size_t out_lo, int n_h,
+                              int hd) {
+  if (nred <= 0) return hipSuccess;
+  dim3 grid(nred, n_h);
+  if (bf16) k_attn_reduce<true><<<grid, hd, 0, st>>>(red, pacc, pml, out, out_lo, n_h, hd);
+  else k_attn_reduce<false><<<grid, hd, 0, st>>>(red, pacc, pml, out, out_lo, n_h, hd);
+  return hipGetLastError();
+}
+
+hipError_t launch_argmax(hipStream_t st, const float* logits, int R, int V, const int* lm_dst, int* tok_store) {
+  if (R <= 0) return hipSuccess;
+  k_argmax<<<R, 256, 0, st>>>(logits, V, lm_dst, tok_store);
+  return hipGetLastError();
+}
+
+}  // namespace moa

@@ -1,0 +1,157 @@
+"""Python-side handle on the C-ABI engine plus the host feeder.
+
+PyTorch only supplies the device arena and the stream. The feeder is the
+plain host-side policy of the paper's setting (Section "Problem Setting": a
+fixed batch of routed calls; Section "MOSAIC: Adaptive Aggregation": the
+aggregator runs on the query plus the expert outputs): it submits the expert
+calls in first-seen order (queries ascending, experts ascending) and, after
+each step, collects what retired one step earlier and submits the aggregator
+call of every query whose experts are all done (ascending query id), on
+query ++ outputs in ascending expert order.
+"""
+import numpy as np
+
+from . import moa as M
+
+
+def model_cfg(shape):
+    return M.moa_model_cfg(shape.n_layers, shape.d_model, shape.n_heads, shape.n_kv_heads,
+                           shape.head_dim, shape.ffn_dim, shape.vocab, shape.rope_theta, shape.rms_eps)
+
+
+def engine_cfg(shape, dtype, consts, max_models, plan_only=False, token_store=0, block_store=0):
+    return M.moa_engine_cfg(model_cfg(shape), M.MOA_BF16 if dtype == "bf16" else M.MOA_F32,
+                            consts.kv_block_size, consts.num_kv_blocks, consts.max_num_seqs,
+                            consts.max_prefill_tokens, consts.max_model_len, max_models,
+                            M.MOA_FLAG_PLAN_ONLY if plan_only else 0, token_store, block_store)
+
+
+class Engine:
+    """Owns one moa_engine and (unless plan_only) its torch-allocated arena."""
+
+    def __init__(self, shape, dtype, consts, max_models, plan_only=False, device="cuda:0",
+                 token_store=0, block_store=0):
+        self.shape = shape
+        self.cfg = engine_cfg(shape, dtype, consts, max_models, plan_only, token_store, block_store)
+        self.arena_bytes = M.moa_arena_bytes(self.cfg)
+        self.plan_only = plan_only
+        self.arena = None
+        if plan_only:
+            self.h = M.moa_create(self.cfg, None, 0, None)
+        else:
+            import torch
+            if not torch.cuda.is_available():
+                raise RuntimeError("the HIP engine needs a GPU (torch.cuda.is_available() is False)")
+            self.device = torch.device(device)
+            self.arena = torch.empty(self.arena_bytes, dtype=torch.uint8, device=self.device)
+            self.stream = torch.cuda.current_stream(self.device)
+            self.h = M.moa_create(self.cfg, self.arena.data_ptr(), self.arena_bytes, self.stream.cuda_stream)
+
+    def load(self, blob):
+        return M.moa_load_expert(self.h, self.cfg.model, np.ascontiguousarray(blob))
+
+    def submit(self, tokens, model_id, max_new):
+        return M.moa_submit(self.h, tokens, model_id, max_new)
+
+    def step(self):
+        return M.moa_step(self.h)
+
+    def collect(self, upto=-1):
+        return M.moa_collect(self.h, upto)
+
+    def sync(self):
+        M.moa_sync(self.h)
+
+    def steps(self):
+        return M.moa_debug_steps(self.h)
+
+    def request(self, rid):
+        return M.moa_debug_request(self.h, rid)
+
+    def block_table(self, rid):
+        return M.moa_debug_block_table(self.h, rid)
+
+    def chunks(self, rid):
+        return M.moa_debug_chunks(self.h, rid)
+
+    def capture_logits(self, rid, arr):
+        M.moa_debug_capture_logits(self.h, rid, arr)
+
+    def close(self):
+        if getattr(self, "h", None) is not None:
+            M.moa_destroy(self.h)
+            self.h = None
+        self.arena = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class FeedResult:
+    def __init__(self):
+        self.outputs = {}        # (q, model_id) -> np.int32 tokens
+        self.rid_of = {}         # (q, model_id) -> request id
+        self.collects = []       # (after_step, [request ids])
+        self.n_steps = 0
+        self.tokens = 0
+
+
+def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None):
+    """Drive ``eng`` through ``workload`` (a moa_inputs.Workload).
+
+    expert_models[e] is the engine model id of expert e; agg_model is the
+    aggregator's model id (-1: none). A workload without experts sends every
+    query straight to the aggregator."""
+    res = FeedResult()
+    who = {}
+    for q, e, G in workload.expert_requests():
+        rid = eng.submit(workload.prompts[q], expert_models[e], G)
+        res.rid_of[(q, expert_models[e])] = rid
+        who[rid] = (q, expert_models[e], e)
+    remaining = {q: len(ex) for q, ex in enumerate(workload.experts) if ex} if agg_model >= 0 else {}
+    if agg_model >= 0 and workload.n_experts == 0:
+        for q in range(workload.n_queries):
+            rid = eng.submit(workload.prompts[q], agg_model, workload.agg_max_new)
+            res.rid_of[(q, agg_model)] = rid
+            who[rid] = (q, agg_model, -1)
+
+    def handle(done, after):
+        if done:
+            res.collects.append((after, [d[0] for d in done]))
+        ready = []
+        for rid, mdl, fin, toks in done:
+            q, m, e = who[rid]
+            res.outputs[(q, m)] = toks
+            res.tokens += len(toks)
+            if q in remaining and e >= 0:
+                remaining[q] -= 1
+                if remaining[q] == 0:
+                    ready.append(q)
+        for q in sorted(ready):
+            parts = [workload.prompts[q]] + [res.outputs[(q, expert_models[e])] for e in workload.experts[q]]
+            rid = eng.submit(np.concatenate(parts).astype(np.int32), agg_model, workload.agg_max_new)
+            res.rid_of[(q, agg_model)] = rid
+            who[rid] = (q, agg_model, -1)
+            del remaining[q]
+        return len(ready)
+
+    last = -1
+    while True:
+        info = eng.step()
+        if info.step < 0:
+            n = handle(eng.collect(last), last)
+            if n == 0:
+                break
+            continue
+        last = info.step
+        res.n_steps += 1
+        if on_step is not None:
+            on_step(info)
+        if last >= 1:
+            handle(eng.collect(last - 1), last - 1)
+        if max_steps is not None and res.n_steps >= max_steps:
+            break
+    return res

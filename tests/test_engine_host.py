@@ -1,0 +1,226 @@
+"""Host-side tests of the C-ABI library (no GPU): symbols, argument checks, and
+the engine's step bookkeeping against the oracle scheduler (dry-run mode)."""
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+
+from moa_inputs import CONFIGS, ModelShape, make_workload
+from moa_inputs.configs import EngineConsts
+from oracle.scheduler import OracleScheduler, run_feeder as oracle_feeder
+from paper_2606_03014_amd import Engine, run_feeder
+from paper_2606_03014_amd import moa as M
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLD = json.load(open(os.path.join(ROOT, "tests", "golden", "step_rule_examples.json")))
+TOY = ModelShape(1, 128, 2, 2, 64, 128, 256)
+
+
+def _blob_bytes(shape, dtype):
+    return shape.n_params() * (2 if dtype == "bf16" else 4)
+
+
+def _dry(shape, consts, n_models, dtype="bf16"):
+    eng = Engine(shape, dtype, consts, max(n_models, 1), plan_only=True)
+    for _ in range(n_models):
+        eng.load(np.zeros(_blob_bytes(shape, dtype), dtype=np.uint8))
+    return eng
+
+
+def test_library_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "moa.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    declared = set(re.findall(r"\b(moa_[a-z_]+)\s*\(", hdr))
+    assert len(declared) >= 14
+    lib = M.lib()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert declared == set(M.exported_symbols())
+
+
+def test_status_strings():
+    for code in (0, -1, -2, -3, -4, -5):
+        assert M.moa_status_str(code).startswith(M.STATUS_NAMES[code])
+
+
+def test_config_validation_and_arena_size():
+    c = CONFIGS["moa-4x1b-bf16"]
+    from paper_2606_03014_amd.engine import engine_cfg
+    good = engine_cfg(c.model, "bf16", c.engine, 4)
+    n = M.moa_arena_bytes(good)
+    weights = 4 * c.model.n_params() * 2
+    kv = c.engine.num_kv_blocks * c.model.n_layers * c.model.n_kv_heads * 2 * 16 * c.model.head_dim * 2
+    assert weights + kv < n < weights + kv + (8 << 30)
+    for field, bad in [("kv_block_size", 32), ("max_models", 0), ("max_models", 9), ("dtype", 7)]:
+        cfg = engine_cfg(c.model, "bf16", c.engine, 4)
+        setattr(cfg, field, bad)
+        with pytest.raises(M.MoaError) as e:
+            M.moa_arena_bytes(cfg)
+        assert e.value.code == M.MOA_EINVAL
+    cfg = engine_cfg(c.model, "bf16", c.engine, 4)
+    cfg.model.head_dim = 96
+    with pytest.raises(M.MoaError):
+        M.moa_arena_bytes(cfg)
+
+
+def test_create_rejects_small_or_missing_arena():
+    c = CONFIGS["tiny-moa-fp32"]
+    from paper_2606_03014_amd.engine import engine_cfg
+    cfg = engine_cfg(c.model, "f32", c.engine, 3)
+    with pytest.raises(M.MoaError) as e:
+        M.moa_create(cfg, None, 0, None)
+    assert e.value.code == M.MOA_EINVAL
+    with pytest.raises(M.MoaError) as e:
+        M.moa_create(cfg, 1 << 20, 4096, None)          # never dereferenced: size check first
+    assert e.value.code == M.MOA_ENOMEM
+
+
+def test_submit_and_load_errors():
+    consts = EngineConsts(num_kv_blocks=4, max_num_seqs=2, max_prefill_tokens=16, max_model_len=100)
+    eng = _dry(TOY, consts, 1)
+    with pytest.raises(M.MoaError) as e:
+        eng.load(np.zeros(10, dtype=np.uint8))
+    assert e.value.code == M.MOA_EINVAL
+    for args, code in [(([1, 2], 1, 3), M.MOA_EINVAL), (([], 0, 3), M.MOA_EINVAL),
+                       (([1, 2], 0, 0), M.MOA_EINVAL), (([1] * 60, 0, 6), M.MOA_ENOSPC),
+                       (([1] * 90, 0, 20), M.MOA_EINVAL)]:
+        with pytest.raises(M.MoaError) as e:
+            eng.submit(*args)
+        assert e.value.code == code, args
+    assert eng.submit([1] * 60, 0, 5) == 0
+    eng.step()
+    with pytest.raises(M.MoaError) as e:
+        eng.load(np.zeros(_blob_bytes(TOY, "bf16"), dtype=np.uint8))
+    assert e.value.code == M.MOA_ESTATE
+
+
+def test_collect_reports_required_capacity():
+    consts = EngineConsts(num_kv_blocks=8, max_num_seqs=4, max_prefill_tokens=64, max_model_len=100)
+    eng = _dry(TOY, consts, 1)
+    for G in (3, 5):
+        eng.submit([1, 2, 3], 0, G)
+    while eng.step().step >= 0:
+        pass
+    import ctypes as C
+    n = C.c_int32()
+    res = (M.moa_result * 1)()
+    buf = np.zeros(4, dtype=np.int32)
+    code = M.lib().moa_collect(eng.h, -1, res, 1, C.byref(n), buf.ctypes.data_as(C.POINTER(C.c_int32)), 4)
+    assert code == M.MOA_EINVAL and n.value == 2
+    out = eng.collect()
+    assert [r[0] for r in out] == [0, 1] and [len(r[3]) for r in out] == [3, 5]
+    assert all((r[3] == -1).all() for r in out)          # a dry run computes no tokens
+    assert eng.collect() == []
+
+
+def test_hand_traced_example_matches():
+    ex = GOLD["examples"][0]
+    consts = EngineConsts(ex["num_blocks"], ex["max_num_seqs"], ex["max_prefill_tokens"], 1000)
+    eng = _dry(TOY, consts, ex["n_models"])
+    for kind, m, P, G in ex["submit"]:
+        assert kind == "std"
+        eng.submit(np.ones(P, dtype=np.int32), m, G)
+    while eng.step().step >= 0:
+        pass
+    st = eng.steps()
+    assert len(st) == ex["n_steps"]
+    assert st[: len(ex["steps_head"])].tolist() == ex["steps_head"]
+    for rid, want in enumerate(ex["requests"]):
+        info = eng.request(rid)
+        assert (info.admit_step, info.finish_step) == (want["admit"], want["finish"])
+        assert eng.block_table(rid) == want["blocks"]
+        assert [list(c) for c in eng.chunks(rid)] == want["chunks"]
+
+
+def test_hand_traced_feeder_matches():
+    f = GOLD["feeder"]
+    consts = EngineConsts(f["num_blocks"], f["max_num_seqs"], f["max_prefill_tokens"], 1000)
+    eng = _dry(TOY, consts, f["n_models"])
+
+    class W:                                          # a two-query workload in the feeder's terms
+        prompts = [np.ones(q["P"], dtype=np.int32) for q in f["queries"]]
+        experts = [tuple(e for e, _ in q["experts"]) for q in f["queries"]]
+        max_new = {(qi, e): G for qi, q in enumerate(f["queries"]) for e, G in q["experts"]}
+        n_experts = 2
+        n_queries = 2
+        agg_max_new = f["agg_G"]
+
+        def expert_requests(self):
+            return [(q, e, self.max_new[(q, e)]) for q in range(2) for e in self.experts[q]]
+
+    r = run_feeder(eng, W(), [0, 1], agg_model=f["aggregator"])
+    assert eng.steps().tolist() == f["steps"]
+    assert [[a, list(b)] for a, b in r.collects] == f["collects"]
+    for rid, want in enumerate(f["requests"]):
+        info = eng.request(rid)
+        assert (info.model_id, info.prompt_len, info.max_new_tokens, info.admit_step, info.finish_step) == (
+            want["model"], want["P"], want["G"], want["admit"], want["finish"])
+        assert eng.block_table(rid) == want["blocks"]
+
+
+def _compare_full(name, seed=0):
+    c = CONFIGS[name]
+    w = make_workload(name, seed)
+    nm = c.n_experts + (1 if c.aggregator else 0)
+    eng = _dry(c.model, c.engine, nm, c.dtype)
+    agg = c.n_experts if c.aggregator else -1
+    r = run_feeder(eng, w, list(range(c.n_experts)), agg_model=agg)
+    s = OracleScheduler(c.engine.num_kv_blocks, c.engine.max_num_seqs, c.engine.max_prefill_tokens, nm,
+                        max_model_len=c.engine.max_model_len)
+    calls = [(q, e, len(w.prompts[q]), G) for q, e, G in w.expert_requests()]
+    direct = [(q, 0, len(w.prompts[q]), w.agg_max_new) for q in range(w.n_queries)] if c.n_experts == 0 else []
+    log, rid_of = oracle_feeder(s, calls, agg_model=agg if c.n_experts else -1, agg_G=w.agg_max_new,
+                                query_len=[len(p) for p in w.prompts], query_experts=w.experts,
+                                direct_calls=direct)
+    assert np.array_equal(eng.steps(), np.array(s.steps, dtype=np.int64))
+    assert [(a, list(b)) for a, b in r.collects] == [(a, list(b)) for a, b in log]
+    for req in s.reqs[:: max(1, len(s.reqs) // 64)]:
+        info = eng.request(req.rid)
+        assert (info.model_id, info.prompt_len, info.max_new_tokens) == (req.expert, req.P, req.G)
+        assert (info.admit_step, info.finish_step) == (req.admit_step, req.finish_step)
+        assert eng.block_table(req.rid) == req.blocks
+        assert [tuple(x) for x in eng.chunks(req.rid)] == [tuple(x) for x in req.chunks]
+    return r
+
+
+@pytest.mark.parametrize("name", ["tiny-moa-fp32", "moa-4x1b-bf16", "agg-prefill-8b-bf16"])
+def test_full_workload_bookkeeping_is_bit_exact(name):
+    _compare_full(name)
+
+
+@pytest.mark.slow
+def test_full_3p1x8b_bookkeeping_is_bit_exact():
+    r = _compare_full("moa-3+1x8b-bf16")
+    assert r.tokens == 5966555
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_random_small_workloads_bit_exact(seed):
+    rng = np.random.default_rng(1000 + seed)
+    consts = EngineConsts(int(rng.integers(4, 40)), int(rng.integers(1, 6)), int(rng.integers(1, 80)), 200)
+    eng = _dry(TOY, consts, 3)
+    s = OracleScheduler(consts.num_kv_blocks, consts.max_num_seqs, consts.max_prefill_tokens, 3,
+                        max_model_len=200)
+    for _ in range(int(rng.integers(1, 14))):
+        m, P, G = int(rng.integers(0, 3)), int(rng.integers(1, 60)), int(rng.integers(1, 30))
+        try:
+            s.submit(m, P, G)
+            ok = True
+        except Exception:
+            ok = False
+        if ok:
+            eng.submit(np.ones(P, dtype=np.int32), m, G)
+        else:
+            with pytest.raises(M.MoaError):
+                eng.submit(np.ones(P, dtype=np.int32), m, G)
+    while True:
+        a = eng.step().step
+        b = s.step()
+        assert a == (-1 if b is None else b)
+        if b is None:
+            break
+    assert np.array_equal(eng.steps(), np.array(s.steps, dtype=np.int64).reshape(-1, 6))
+    for req in s.reqs:
+        assert eng.block_table(req.rid) == req.blocks

@@ -1,0 +1,154 @@
+"""GPU parity: the HIP engine, called through the C ABI, against the oracle.
+
+Every comparison is teacher-forced: the oracle recomputes each emitted
+position on the engine's own history, so one near-tie never cascades.
+Logit bounds: 1e-4 (fp32 engine) / 2e-2 (bf16 engine) max abs error against
+the pure fp64 oracle. Tokens: identical to the oracle (fp32) or to the
+oracle in bf16-rounding mode (bf16), except where the oracle's top-2 margin
+is below 1e-3.
+"""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+from moa_inputs import CONFIGS, ModelShape, generate_weights, make_workload, pack_blob
+from moa_inputs.configs import EngineConsts, LLAMA_1B, LLAMA_8B
+from oracle import transformer as T
+from paper_2606_03014_amd import Engine, run_feeder
+from tests.gpu_helpers import check_tokens, compare, run_requests, say
+
+pytestmark = pytest.mark.gpu
+
+SMALL_BF16 = ModelShape(n_layers=2, d_model=256, n_heads=8, n_kv_heads=2, head_dim=64, ffn_dim=512, vocab=1024)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need the MI355X"
+
+
+def _prompts(V, lens, seed):
+    rng = np.random.default_rng([seed, 11])
+    return [rng.integers(0, V, n).astype(np.int32) for n in lens]
+
+
+def test_zero_projection_model_is_closed_form_fp32():
+    """Wo = Wdown = 0: every layer leaves the residual alone, so the logits
+    are Wlm . rmsnorm(E[token]) at every position."""
+    c = CONFIGS["tiny-moa-fp32"]
+    w = generate_weights(c.model, "f32", 0, c.wid, 0)
+    for l in range(c.model.n_layers):
+        w[f"layers.{l}.wo"][:] = 0
+        w[f"layers.{l}.w_down"][:] = 0
+    prompts = _prompts(c.model.vocab, [1, 20, 64], 1)
+    say("closed form: 3 requests")
+    toks, logs = run_requests(c.model, "f32", c.engine, [w], [(p, 0, 7) for p in prompts])
+    E = w["embed"].astype(np.float64)
+    Wl = w["lm_head"].astype(np.float64)
+    for p, t, lg in zip(prompts, toks, logs):
+        seq = np.concatenate([p, t[:-1]])[len(p) - 1:]
+        x = E[seq]
+        ref = (x / np.sqrt((x * x).mean(-1, keepdims=True) + c.model.rms_eps)) @ Wl.T
+        assert np.abs(lg - ref).max() <= 1e-4
+        assert list(t) == [int(np.argmax(r)) for r in ref]
+
+
+def test_tiny_workload_full_fp32():
+    """The tiny MoA workload end to end: 32 expert calls and 16 aggregator
+    calls, every position of every call compared with the oracle."""
+    c = CONFIGS["tiny-moa-fp32"]
+    ws = [generate_weights(c.model, "f32", 0, c.wid, m) for m in range(3)]
+    wl = make_workload(c.name, 0)
+    eng = Engine(c.model, "f32", c.engine, 3)
+    mids = [eng.load(pack_blob(w, c.model)) for w in ws]
+    say("tiny workload: running")
+    r = run_feeder(eng, wl, mids[:2], agg_model=mids[2])
+    eng.close()
+    assert r.tokens == wl.total_expert_tokens() + wl.n_queries * wl.agg_max_new
+    models = [T.OracleModel(c.model, w) for w in ws]
+    nflip = 0
+    for (q, m), toks in r.outputs.items():
+        if m < 2:
+            prompt = wl.prompts[q]
+            assert len(toks) == wl.max_new[(q, m)]
+        else:
+            prompt = np.concatenate([wl.prompts[q]] + [r.outputs[(q, e)] for e in wl.experts[q]])
+            assert len(toks) == wl.agg_max_new
+        ref = T.teacher_forced_logits(models[m], prompt, toks)
+        nflip += len(check_tokens(ref, toks, f"q{q} m{m}"))
+    say(f"tiny workload: {len(r.outputs)} calls checked, {nflip} near-tie flips")
+
+
+def test_tiny_logits_fp32_chunked_and_split():
+    """fp32 logits within 1e-4 on prompts that span several prefill chunks
+    (budget 64) and contexts past one 256-key decode split."""
+    c = CONFIGS["tiny-moa-fp32"]
+    consts = EngineConsts(num_kv_blocks=128, max_num_seqs=8, max_prefill_tokens=64, max_model_len=512)
+    ws = [generate_weights(c.model, "f32", 7, c.wid, m) for m in range(2)]
+    prompts = _prompts(c.model.vocab, [3, 64, 65, 250, 300], 2)
+    reqs = [(p, i % 2, G) for i, (p, G) in enumerate(zip(prompts, [40, 9, 20, 30, 12]))]
+    toks, logs = run_requests(c.model, "f32", consts, ws, reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, _ = compare(c.model, ws[m], p, t, lg, False, 1e-4, what=f"req{i}")
+        say(f"fp32 req{i} P={len(p)} G={G}: max err {err:.2e}")
+
+
+def test_bf16_small_ragged_batch():
+    """bf16, GQA 4, two models, ragged prompts (1..300) and decode past one
+    split; exercises 1/2/4-chunk row tiles and split-K."""
+    consts = EngineConsts(num_kv_blocks=256, max_num_seqs=8, max_prefill_tokens=96, max_model_len=512)
+    ws = [generate_weights(SMALL_BF16, "bf16", 3, 99, m) for m in range(2)]
+    prompts = _prompts(SMALL_BF16.vocab, [1, 17, 70, 300, 33, 128], 3)
+    Gs = [30, 12, 25, 8, 40, 3]
+    reqs = [(p, i % 2, G) for i, (p, G) in enumerate(zip(prompts, Gs))]
+    toks, logs = run_requests(SMALL_BF16, "bf16", consts, ws, reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, flips = compare(SMALL_BF16, ws[m], p, t, lg, True, 2e-2, what=f"req{i}")
+        say(f"bf16 small req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+
+
+def test_bf16_runs_are_deterministic():
+    consts = EngineConsts(num_kv_blocks=256, max_num_seqs=8, max_prefill_tokens=96, max_model_len=512)
+    ws = [generate_weights(SMALL_BF16, "bf16", 4, 99, m) for m in range(2)]
+    prompts = _prompts(SMALL_BF16.vocab, [5, 90, 280], 4)
+    reqs = [(p, i % 2, 30) for i, p in enumerate(prompts)]
+    outs, caps = run_requests(SMALL_BF16, "bf16", consts, ws, reqs, repeat=2)
+    for a, b in zip(outs[0], outs[1]):
+        assert np.array_equal(a, b)
+    for a, b in zip(caps[0], caps[1]):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("base,wid", [(LLAMA_1B, 2), (LLAMA_8B, 3)], ids=["1b-width", "8b-width"])
+def test_bf16_real_width_two_layers(base, wid):
+    """Real widths (d, heads, head_dim, ffn, vocab) with two layers: every
+    kernel at its true shape, depth only repeats it."""
+    shape = replace(base, n_layers=2)
+    consts = EngineConsts(num_kv_blocks=512, max_num_seqs=16, max_prefill_tokens=512, max_model_len=2048)
+    say(f"generating {shape.d_model}-wide weights")
+    ws = [generate_weights(base, "bf16", 0, wid, m, n_layers=2) for m in range(2)]
+    prompts = _prompts(shape.vocab, [9, 300, 700], 5)
+    reqs = [(prompts[0], 0, 24), (prompts[1], 1, 6), (prompts[2], 0, 4)]
+    toks, logs = run_requests(shape, "bf16", consts, ws, reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, flips = compare(shape, ws[m], p, t, lg, True, 2e-2, what=f"req{i}")
+        say(f"{shape.d_model}-wide req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+
+
+def test_bf16_1b_full_depth_requests():
+    """The 1B-shape expert at full depth (16 layers): short, median and a
+    long-decode request of the 4x1B workload, teacher-forced."""
+    c = CONFIGS["moa-4x1b-bf16"]
+    wl = make_workload(c.name, 0)
+    w = generate_weights(c.model, "bf16", 0, c.wid, 0)
+    calls = [(q, G) for q, e, G in wl.expert_requests() if e == 0]
+    calls.sort(key=lambda x: len(wl.prompts[x[0]]) + x[1])
+    pick = [calls[0], calls[len(calls) // 2]]
+    consts = EngineConsts(num_kv_blocks=4096, max_num_seqs=8, max_prefill_tokens=4096, max_model_len=c.engine.max_model_len)
+    reqs = [(wl.prompts[q], 0, min(G, 96)) for q, G in pick]
+    toks, logs = run_requests(c.model, "bf16", consts, [w], reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, flips = compare(c.model, w, p, t, lg, True, 2e-2, what=f"1b req{i}")
+        say(f"1b full depth req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")

@@ -118,14 +118,22 @@ def test_decode_from_history_matches_prefill():
     np.testing.assert_allclose(lg, T.forward_full(om, toks)[9], rtol=1e-11, atol=1e-12)
 
 
-def test_bf16_emulation_is_close_but_not_identical():
+def test_bf16_kv_rounds_only_the_cache():
+    """bf16_kv changes the logits only through the stored K/V: a model whose
+    K/V projections produce bf16-representable values is unaffected, and the
+    bf16 weights themselves are read exactly."""
     shape = MINI
     w = generate_weights(shape, "bf16", 0, 99, 0)
     om = T.OracleModel(shape, w)
     toks = _tokens(16, shape.vocab, 8)
     a = T.forward_full(om, toks)
-    b = T.forward_full(om, toks, emulate_bf16=True)
+    b = T.forward_full(om, toks, bf16_kv=True)
     err = np.abs(a - b).max()
     assert 0 < err < 5e-2 * np.abs(a).max()
-    # the bf16 storage itself is read exactly
     np.testing.assert_allclose(a, torch_logits(shape, w, toks), rtol=1e-10, atol=1e-12)
+    w2 = dict(w)
+    for l in range(shape.n_layers):       # zero K/V projections: stored values are exact zeros
+        w2[f"layers.{l}.wk"] = np.zeros_like(w[f"layers.{l}.wk"])
+        w2[f"layers.{l}.wv"] = np.zeros_like(w[f"layers.{l}.wv"])
+    om2 = T.OracleModel(shape, w2)
+    assert np.array_equal(T.forward_full(om2, toks), T.forward_full(om2, toks, bf16_kv=True))
