@@ -192,6 +192,36 @@ moa_status moa_debug_steps(moa_engine* e, int64_t* out, int64_t cap_steps, int64
  * collected. Must be registered before the request's prefill completes. */
 moa_status moa_debug_capture_logits(moa_engine* e, int64_t request_id, float* host_logits);
 
+/* Kernel classes of one step (for moa_debug_time_kernels). */
+enum {
+  MOA_K_EMBED = 0, MOA_K_NORM, MOA_K_GEMM_QKV, MOA_K_ROPE_KV, MOA_K_ATTN, MOA_K_ATTN_REDUCE,
+  MOA_K_GEMM_O, MOA_K_GEMM_GATEUP, MOA_K_GEMM_DOWN, MOA_K_GEMM_LMHEAD, MOA_K_ARGMAX, MOA_K_COUNT
+};
+
+/* Per-class launch statistics of the sampled steps. bytes/flops are the
+ * algorithmic figures of those launches: for a GEMM the bf16 weights it
+ * streams (N*K*2 per model group) plus its split-bf16 input (M*K*4) and fp32
+ * output (M*N*4), flops 2*M*N*K; for attention the bf16 K/V it reads
+ * (keys*2*head_dim*2 per KV head) plus q (fp32) and its output. */
+typedef struct {
+  int64_t launches;   /* timed launches (sampled steps) */
+  double ms;          /* their summed durations (HIP events on the engine's stream) */
+  double bytes;       /* their algorithmic bytes */
+  double flops;       /* their algorithmic flops */
+  int64_t launches_all; /* every launch since the reset */
+  double bytes_all, flops_all;
+  double roof_ms_all; /* sum over every launch of max(bytes / peak_bw, flops / peak_flops) */
+} moa_kernel_stats;
+
+/* Reset the statistics; from now on account every launch (bytes, flops,
+ * roofline time at the given peaks, bytes/s and flop/s) and time every launch
+ * of one step out of `every` (every <= 0: no timing) with an event pair
+ * around it on the engine's stream. */
+moa_status moa_debug_time_kernels(moa_engine* e, int32_t every, double peak_bw, double peak_flops);
+
+/* Statistics per class, out[MOA_K_COUNT]. Waits for the stream. */
+moa_status moa_debug_kernel_stats(moa_engine* e, moa_kernel_stats* out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -106,7 +106,7 @@ bool valid_cfg(const moa_engine_cfg& c) {
   if (gq != 1 && gq != 2 && gq != 4 && gq != 8) return false;
   if (m.head_dim != 64 && m.head_dim != 128) return false;
   if (!(m.rms_eps > 0.f) || !(m.rope_theta > 0.f)) return false;
-  if (m.d_model % 64 || m.ffn_dim % 64 || m.vocab % 16) return false;
+  if (m.d_model % 256 || m.d_model > 4096 || m.ffn_dim % 64 || m.vocab % 16) return false;
   if (c.dtype == MOA_F32 && (m.vocab % 64 || (2 * m.ffn_dim) % 64)) return false;
   // bf16 GEMMs stream K in batches of 4 MFMA k-steps of 32
   if (c.dtype == MOA_BF16 && (m.d_model % 128 || m.ffn_dim % 128 || (m.n_heads * m.head_dim) % 128)) return false;
@@ -210,6 +210,16 @@ struct moa_engine {
   int32_t* pinned_out = nullptr;
   size_t pinned_out_cap = 0;
 
+  // kernel timing (inspection hook): event pairs around launches of sampled steps
+  struct Timed { int cls; hipEvent_t a, b; double bytes, flops; };
+  int time_every = 0;
+  bool time_now = false;
+  bool account = false;
+  double peak_bw = 8e12, peak_flops = 2.5e15;
+  std::vector<hipEvent_t> ev_pool;
+  std::vector<Timed> timed;
+  moa_kernel_stats kstats[MOA_K_COUNT] = {};
+
   // per-step host plan (reused vectors)
   std::vector<int> r_tok, r_pos, r_bt, r_model, l_src, l_dst;
   std::vector<AttnItem> items;
@@ -228,6 +238,66 @@ moa_status hip_fail(moa_engine* e, hipError_t err, const char* what) {
   do {                                                  \
     hipError_t _err = (call);                           \
     if (_err != hipSuccess) return hip_fail(e, _err, what); \
+  } while (0)
+
+hipEvent_t pool_event(moa_engine* e) {
+  if (!e->ev_pool.empty()) {
+    hipEvent_t v = e->ev_pool.back();
+    e->ev_pool.pop_back();
+    return v;
+  }
+  hipEvent_t v = nullptr;
+  if (hipEventCreate(&v) != hipSuccess) return nullptr;
+  return v;
+}
+
+// Fold finished timing pairs into the statistics (waits for each pair).
+moa_status resolve_timed(moa_engine* e) {
+  for (auto& t : e->timed) {
+    HIPCHK(hipEventSynchronize(t.b), "timing wait");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, t.a, t.b) != hipSuccess) {   // launch carried no work
+      (void)hipGetLastError();
+      e->ev_pool.push_back(t.a);
+      e->ev_pool.push_back(t.b);
+      continue;
+    }
+    moa_kernel_stats& k = e->kstats[t.cls];
+    k.launches += 1;
+    k.ms += ms;
+    k.bytes += t.bytes;
+    k.flops += t.flops;
+    e->ev_pool.push_back(t.a);
+    e->ev_pool.push_back(t.b);
+  }
+  e->timed.clear();
+  return MOA_OK;
+}
+
+// Launch `call` (an expression yielding hipError_t). Every launch is
+// accounted (algorithmic bytes, flops, roofline time); in sampled steps the
+// kernel's own dispatch also carries a start/stop event pair.
+#define LAUNCH(cls, bytes_, flops_, call, what)                                   \
+  do {                                                                           \
+    if (e->account) {                                                            \
+      moa_kernel_stats& _k = e->kstats[(cls)];                                   \
+      const double _by = (double)(bytes_), _fl = (double)(flops_);               \
+      _k.launches_all += 1;                                                      \
+      _k.bytes_all += _by;                                                       \
+      _k.flops_all += _fl;                                                       \
+      _k.roof_ms_all += 1e3 * std::max(_by / e->peak_bw, _fl / e->peak_flops);   \
+    }                                                                            \
+    if (e->time_now) {                                                           \
+      hipEvent_t _a = pool_event(e), _b = pool_event(e);                         \
+      if (!_a || !_b) return hip_fail(e, hipErrorOutOfMemory, "timing events");  \
+      set_launch_events(_a, _b);                                                 \
+      hipError_t _err = (call);                                                  \
+      set_launch_events(nullptr, nullptr);                                       \
+      if (_err != hipSuccess) return hip_fail(e, _err, what);                    \
+      e->timed.push_back({(cls), _a, _b, (double)(bytes_), (double)(flops_)});  \
+    } else {                                                                     \
+      HIPCHK((call), what);                                                      \
+    }                                                                            \
   } while (0)
 
 // Tile-shuffle a row-major [N][K] bf16 matrix into MFMA B-fragment order:
@@ -287,15 +357,26 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     a.S = 1; a.ksteps = 0; a.out_split = 0; a.total_items = item;
     return;
   }
-  mt = maxM <= 16 ? 1 : (maxM <= 32 ? 2 : 4);
-  nt = (epi == EPI_SWIGLU) ? 2 : 1;
-  const int tiles = N / 16 / nt;
   const int KS = K / 32;
-  int base = 0;
-  for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 16 * mt - 1) / (16 * mt)) * tiles;
+  const bool row_block = maxM > 32 && N % 128 == 0;
+  int tiles, rows_per, target, base = 0;
+  if (row_block) {          // workgroup items: 64 rows x 128 columns
+    mt = kRowBlock;
+    nt = 2;
+    tiles = N / 128;
+    rows_per = 64;
+    target = kTargetWaves / 4;
+  } else {                  // wavefront items: 16*mt rows x 16*nt columns
+    mt = maxM <= 16 ? 1 : (maxM <= 32 ? 2 : 4);
+    nt = (epi == EPI_SWIGLU) ? 2 : 1;
+    tiles = N / 16 / nt;
+    rows_per = 16 * mt;
+    target = kTargetWaves;
+  }
+  for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + rows_per - 1) / rows_per) * tiles;
   int S = 1;
   if (allow_split) {
-    while (base * S < kTargetWaves && KS % (S * 2 * 8) == 0 &&
+    while (base * S < target && KS % (S * 2 * 8) == 0 &&
            (int64_t)S * 2 * totalM * N <= e->lay.part_cap && S < 16)
       S *= 2;
   }
@@ -305,7 +386,7 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
   int item = 0;
   for (int g = 0; g < in.ngroups; ++g) {
     a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
-    a.g[g].n_mc = (in.nrows[g] + 16 * mt - 1) / (16 * mt);
+    a.g[g].n_mc = (in.nrows[g] + rows_per - 1) / rows_per;
     a.g[g].item0 = item;
     item += a.g[g].n_mc * S * tiles;
   }
@@ -407,6 +488,8 @@ void moa_destroy(moa_engine* e) {
       if (e->ev[i]) (void)hipEventDestroy(e->ev[i]);
     }
     if (e->pinned_out) (void)hipHostFree(e->pinned_out);
+    for (auto& t : e->timed) { (void)hipEventDestroy(t.a); (void)hipEventDestroy(t.b); }
+    for (hipEvent_t v : e->ev_pool) (void)hipEventDestroy(v);
     if (e->copy_stream) (void)hipStreamDestroy(e->copy_stream);
   }
   delete e;
@@ -563,6 +646,12 @@ moa_status ensure_stage(moa_engine* e, int slot, size_t bytes) {
   return MOA_OK;
 }
 
+int64_t nslots_total(const moa_engine* e) {
+  int64_t n = 0;
+  for (const ReduceItem& r : e->red) n += r.nslots;
+  return n;
+}
+
 moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int T, int R,
                         const int* grp_rows, const int* grp_lm) {
   const moa_model_cfg& g = e->cfg.model;
@@ -640,50 +729,84 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   }
   auto weights = [&](auto get) { GemmPlanIn w = gin; for (int k = 0; k < w.ngroups; ++k) w.W[k] = get(e->models[gmodel[k]]); return w; };
 
+  e->time_now = e->time_every > 0 && (e->step_idx % e->time_every) == 0;
+  if (e->time_now && e->timed.size() > 16384) {
+    moa_status rs = resolve_timed(e);
+    if (rs != MOA_OK) return rs;
+  }
+  const double esz = (double)L.esz;
+  // algorithmic bytes / flops of one grouped GEMM launch
+  auto gemm_cost = [&](const GemmArgs& a, int epi, double& bytes, double& flops) {
+    double rows = 0;
+    for (int k = 0; k < a.ngroups; ++k) rows += a.g[k].nrows;
+    const double out_elems = epi == EPI_SWIGLU ? rows * a.N / 2 : rows * a.N;
+    bytes = a.ngroups * (double)a.N * a.K * esz + rows * a.K * 4.0 + out_elems * 4.0;
+    flops = 2.0 * rows * a.N * a.K;
+  };
+  double kv_keys = 0;
+  for (const AttnItem& it : e->items) kv_keys += it.k1 - it.k0;
+  const double attn_bytes = kv_keys * nkv * 2.0 * hd * esz + (double)T * nh * hd * 8.0;
+  const double attn_flops = kv_keys * nh * hd * 4.0;
+  const double norm_bytes = (double)T * d * 12.0;
+  double gb = 0, gf = 0;
+
   if (T > 0) {
-    HIPCHK(launch_embed(s, bf, e->tok_store, sd.row_tok, sd.row_model, fill([](const ModelDev& x) { return x.embed; }),
-                        e->x, T, d), "embed");
+    LAUNCH(MOA_K_EMBED, (double)T * d * (4.0 + esz), 0,
+           launch_embed(s, bf, e->tok_store, sd.row_tok, sd.row_model,
+                        fill([](const ModelDev& x) { return x.embed; }), e->x, T, d), "embed");
     int prev_split = 0;
     size_t prev_stride = 0;
     for (int l = 0; l < g.n_layers; ++l) {
       GemmArgs ga;
       int mt, nt;
-      HIPCHK(launch_add_rmsnorm(s, bf, e->x, prev_split ? e->part : nullptr, prev_split, prev_stride, nullptr,
+      LAUNCH(MOA_K_NORM, norm_bytes + prev_split * (double)T * d * 4.0, 0,
+             launch_add_rmsnorm(s, bf, e->x, prev_split ? e->part : nullptr, prev_split, prev_stride, nullptr,
                                 sd.row_model, T, fill([l](const ModelDev& x) { return x.attn_norm[l]; }), e->xn,
                                 xn_lo, d, g.rms_eps), "attn norm");
       plan_gemm(e, weights([l](const ModelDev& x) { return x.wqkv[l]; }), d, qkv, EPI_F32, e->xn, xn_lo, e->part,
                 nullptr, 0, true, ga, mt, nt);
-      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "qkv gemm");
-      HIPCHK(launch_rope_kv(s, bf, e->part, ga.S, ga.out_split, sd.row_pos, sd.row_bt, e->bt_store, e->rope, e->q,
+      gemm_cost(ga, EPI_F32, gb, gf);
+      LAUNCH(MOA_K_GEMM_QKV, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "qkv gemm");
+      LAUNCH(MOA_K_ROPE_KV, (double)T * qkv * 4.0 * ga.S + (double)T * (nh * hd * 4.0 + 2.0 * nkv * hd * esz), 0,
+             launch_rope_kv(s, bf, e->part, ga.S, ga.out_split, sd.row_pos, sd.row_bt, e->bt_store, e->rope, e->q,
                             e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd, T), "rope kv");
-      HIPCHK(launch_attention(s, bf, sd.items, nitems, e->q, e->kv, e->bt_store, sd.row_bt, l, e->cfg.num_kv_blocks,
-                              nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc, e->pml),
-             "attention");
-      HIPCHK(launch_attn_reduce(s, bf, sd.red, nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
+      LAUNCH(MOA_K_ATTN, attn_bytes, attn_flops,
+             launch_attention(s, bf, sd.items, nitems, e->q, e->kv, e->bt_store, sd.row_bt, l,
+                              e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc,
+                              e->pml), "attention");
+      if (nred > 0)
+        LAUNCH(MOA_K_ATTN_REDUCE, (double)nslots_total(e) * nh * (hd + 2) * 4.0, 0,
+               launch_attn_reduce(s, bf, sd.red, nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
       plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), nh * hd, d, EPI_F32, e->ao, ao_lo, e->part,
                 nullptr, 0, true, ga, mt, nt);
-      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "o gemm");
-      HIPCHK(launch_add_rmsnorm(s, bf, e->x, e->part, ga.S, ga.out_split, nullptr, sd.row_model, T,
+      gemm_cost(ga, EPI_F32, gb, gf);
+      LAUNCH(MOA_K_GEMM_O, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "o gemm");
+      LAUNCH(MOA_K_NORM, norm_bytes + ga.S * (double)T * d * 4.0, 0,
+             launch_add_rmsnorm(s, bf, e->x, e->part, ga.S, ga.out_split, nullptr, sd.row_model, T,
                                 fill([l](const ModelDev& x) { return x.mlp_norm[l]; }), e->xn, xn_lo, d,
                                 g.rms_eps), "mlp norm");
       if (bf) {
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), d, 2 * F, EPI_SWIGLU, e->xn, xn_lo,
                   nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt);
-        HIPCHK(launch_gemm(s, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
+        gemm_cost(ga, EPI_SWIGLU, gb, gf);
+        LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(s, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
       } else {
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), d, 2 * F, EPI_F32, e->xn, 0, e->part,
                   nullptr, 0, false, ga, mt, nt);
-        HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
+        gemm_cost(ga, EPI_F32, gb, gf);
+        LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
         HIPCHK(launch_swiglu_f32(s, e->part, (float*)e->h, T, F), "swiglu");
       }
       plan_gemm(e, weights([l](const ModelDev& x) { return x.wdown[l]; }), F, d, EPI_F32, e->h, h_lo, e->part,
                 nullptr, 0, true, ga, mt, nt);
-      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "down gemm");
+      gemm_cost(ga, EPI_F32, gb, gf);
+      LAUNCH(MOA_K_GEMM_DOWN, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "down gemm");
       prev_split = ga.S;
       prev_stride = ga.out_split;
     }
     if (R > 0) {
-      HIPCHK(launch_add_rmsnorm(s, bf, e->x, e->part, prev_split, prev_stride, sd.lm_src, sd.row_model, R,
+      LAUNCH(MOA_K_NORM, (double)R * d * (12.0 + prev_split * 4.0), 0,
+             launch_add_rmsnorm(s, bf, e->x, e->part, prev_split, prev_stride, sd.lm_src, sd.row_model, R,
                                 fill([](const ModelDev& x) { return x.final_norm; }), e->xn, xn_lo, d,
                                 g.rms_eps), "final norm");
       GemmPlanIn lin;
@@ -699,8 +822,10 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
       GemmArgs ga;
       int mt, nt;
       plan_gemm(e, lin, d, V, EPI_F32, e->xn, xn_lo, e->logits, nullptr, 0, false, ga, mt, nt);
-      HIPCHK(launch_gemm(s, bf, ga, EPI_F32, mt, nt), "lm head");
-      HIPCHK(launch_argmax(s, e->logits, R, V, sd.lm_dst, e->tok_store), "argmax");
+      gemm_cost(ga, EPI_F32, gb, gf);
+      LAUNCH(MOA_K_GEMM_LMHEAD, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "lm head");
+      LAUNCH(MOA_K_ARGMAX, (double)R * V * 4.0, 0, launch_argmax(s, e->logits, R, V, sd.lm_dst, e->tok_store),
+             "argmax");
     }
   }
   (void)L;
@@ -972,6 +1097,32 @@ moa_status moa_debug_steps(moa_engine* e, int64_t* out, int64_t cap, int64_t* n_
   if ((int64_t)e->trace.size() > cap || (!out && !e->trace.empty())) return MOA_EINVAL;
   for (size_t i = 0; i < e->trace.size(); ++i)
     for (int k = 0; k < 6; ++k) out[6 * i + k] = e->trace[i][k];
+  return MOA_OK;
+}
+
+moa_status moa_debug_time_kernels(moa_engine* e, int32_t every, double peak_bw, double peak_flops) {
+  if (!e || !(peak_bw > 0) || !(peak_flops > 0)) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (!e->plan_only) {
+    moa_status st = resolve_timed(e);
+    if (st != MOA_OK) return st;
+  }
+  e->time_every = e->plan_only ? 0 : std::max(0, every);
+  e->account = true;
+  e->peak_bw = peak_bw;
+  e->peak_flops = peak_flops;
+  for (auto& k : e->kstats) k = moa_kernel_stats{};
+  return MOA_OK;
+}
+
+moa_status moa_debug_kernel_stats(moa_engine* e, moa_kernel_stats* out) {
+  if (!e || !out) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (!e->plan_only) {
+    moa_status st = resolve_timed(e);
+    if (st != MOA_OK) return st;
+  }
+  for (int i = 0; i < MOA_K_COUNT; ++i) out[i] = e->kstats[i];
   return MOA_OK;
 }
 

@@ -40,6 +40,10 @@ struct GemmArgs {
 
 enum Epilogue { EPI_F32 = 0, EPI_SWIGLU = 1 };
 
+// launch_gemm(mt = kRowBlock): the LDS row-block kernel; each GemmArgs item is
+// one workgroup of 64 rows x 128 columns x one k-split (N % 128 == 0).
+constexpr int kRowBlock = 64;
+
 // Attention work item: one query row against keys [k0, k1) of its request.
 struct AttnItem { int row, k0, k1, slot; };   // slot < 0: write the final output
 struct ReduceItem { int row, slot0, nslots, pad; };
@@ -54,6 +58,9 @@ struct StepDev {
   const AttnItem* items; // attention items
   const ReduceItem* red; // split-combine items
 };
+
+// Attach a start/stop event pair to the launches that follow (nullptr: none).
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
 
 // All launchers enqueue on `st` and return hipGetLastError().
 hipError_t launch_embed(hipStream_t st, bool bf16, const int* tok_store, const int* row_tok,

@@ -8,11 +8,29 @@
 // v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <climits>
 #include <cmath>
 
 namespace moa {
+
+// Optional event pair attached to the next launch (hipExtLaunchKernel
+// timestamps the dispatch itself, so the measured span is the kernel's).
+static hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+void set_launch_events(hipEvent_t start, hipEvent_t stop) {
+  g_ev_start = start;
+  g_ev_stop = stop;
+}
+
+template <typename... KArgs, typename... Args>
+static void klaunch(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t st, Args... args) {
+  if (g_ev_start)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, g_ev_start, g_ev_stop, 0, args...);
+  else
+    kernel<<<grid, block, 0, st>>>(args...);
+}
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -85,34 +103,49 @@ __global__ __launch_bounds__(256) void k_embed(const int* __restrict__ tok_store
 // ------------------------------------------------- residual add + RMSNorm
 // x[r] += sum_s part[s][r] (split-K partial sums of the previous projection),
 // out[j] = x[r] * rsqrt(mean(x[r]^2) + eps) * gamma, r = gather ? gather[j] : j.
+// One workgroup per row, one float4 of the row per thread (blockDim = d/4);
+// the partial-sum loads of a thread are all in flight before they are added.
 template <bool BF>
-__global__ __launch_bounds__(256) void k_add_rmsnorm(float* __restrict__ x, const float* __restrict__ part,
-                                                     int nsplit, size_t split_stride,
-                                                     const int* __restrict__ gather,
-                                                     const int* __restrict__ row_model, ModelPtrs gamma,
-                                                     void* __restrict__ out, size_t out_lo, int d, float eps) {
-  __shared__ float red[4];
+__global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, const float* __restrict__ part,
+                                                      int nsplit, size_t split_stride,
+                                                      const int* __restrict__ gather,
+                                                      const int* __restrict__ row_model, ModelPtrs gamma,
+                                                      void* __restrict__ out, size_t out_lo, int d, float eps) {
+  __shared__ float red[16];
   const int j = blockIdx.x;
   const int r = gather ? gather[j] : j;
-  float* xr = x + (size_t)r * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float v = xr[i];
-    for (int s = 0; s < nsplit; ++s) v += part[(size_t)s * split_stride + (size_t)r * d + i];
-    if (nsplit) xr[i] = v;
-    ss += v * v;
+  const int i = threadIdx.x * 4;
+  float4* xr = (float4*)(x + (size_t)r * d + i);
+  float4 v = *xr;
+  if (nsplit) {
+    const float* pp = part + (size_t)r * d + i;
+#pragma unroll 16
+    for (int s = 0; s < nsplit; ++s) {
+      const float4 p = *(const float4*)(pp + (size_t)s * split_stride);
+      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+    }
+    *xr = v;
   }
-  ss = block_sum256(ss, red);
-  const float scale = rsqrtf(ss / (float)d + eps);
+  float ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  ss = wave_sum(ss);
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = ss;
+  __syncthreads();
+  float tot = 0.f;
+  for (int k = 0; k < nw; ++k) tot += red[k];
+  const float scale = rsqrtf(tot / (float)d + eps);
   const void* g = pick(gamma, row_model[r]);
+  const float y[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
   if (BF) {
-    uint16_t* o = (uint16_t*)out + (size_t)j * d;
-    const uint16_t* gg = (const uint16_t*)g;
-    for (int i = threadIdx.x; i < d; i += 256) store_split(o, out_lo, i, xr[i] * scale * bf2f(gg[i]));
+    uint16_t* o = (uint16_t*)out + (size_t)j * d + i;
+    const uint16_t* gg = (const uint16_t*)g + i;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) store_split(o, out_lo, k, y[k] * bf2f(gg[k]));
   } else {
-    float* o = (float*)out + (size_t)j * d;
-    const float* gg = (const float*)g;
-    for (int i = threadIdx.x; i < d; i += 256) o[i] = xr[i] * scale * gg[i];
+    float* o = (float*)out + (size_t)j * d + i;
+    const float* gg = (const float*)g + i;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = y[k] * gg[k];
   }
 }
 
@@ -233,6 +266,129 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs a) {
   }
 }
 
+// ------------------------------------------- bf16 GEMM, row-block variant
+// For groups with more than 32 rows. A workgroup (4 wavefronts) owns 64 rows
+// x 128 columns x one k-split: the split-bf16 activation block (64 rows, both
+// planes) is staged once per 128-wide k stage in LDS, laid out in MFMA
+// A-fragment order (one 1 KB lane-ordered fragment per 16 rows x 32 k x plane,
+// so fragment reads are contiguous), and each wavefront streams its own two
+// 16-column weight tiles from HBM. Activation traffic is thus paid per
+// workgroup instead of per wavefront. Workgroup ids are remapped so that
+// consecutive logical blocks -- the row chunks that share weight tiles -- run
+// on the same XCD and share its L2.
+constexpr int kRB_UK = 4;                       // k-steps (of 32) per LDS stage
+constexpr int kRB_FRAG = 64 * 16;               // bytes per fragment
+constexpr int kRB_STAGE = 2 * 4 * kRB_UK * kRB_FRAG;   // planes x m-tiles x k-steps
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_bf16_rb(GemmArgs a, int nwg) {
+  __shared__ __align__(16) unsigned char sA[kRB_STAGE];
+  // XCD-aware remap: physical workgroup p runs on XCD p % 8
+  const int per = (nwg + 7) / 8;
+  const int blk = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (blk >= a.total_items) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const void* Wg = a.g[0].W;
+  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroups; ++i) {
+    if (i < a.ngroups && a.g[i].item0 <= blk) {
+      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
+    }
+  }
+  const int idx = blk - item0;
+  const int mc = idx % n_mc;
+  const int rest = idx / n_mc;
+  const int s = rest % a.S;
+  const int nb = rest / a.S;
+  const int ks0 = s * a.ksteps;
+  const int nt0 = nb * 8 + w * 2;             // this wavefront's two 16-column tiles
+  const int KS = a.K >> 5;
+  const uint4* W = (const uint4*)Wg;
+  const uint4* wp0 = W + ((size_t)nt0 * KS + ks0) * 64 + lane;
+  const uint4* wp1 = W + ((size_t)(nt0 + 1) * KS + ks0) * 64 + lane;
+  const int rbase = row0 + mc * 64;
+  const int rend = row0 + nrows;
+
+  // staging map: thread t moves 16-byte units u = t + 256*i (i < 8) of the
+  // stage: plane p = u / 1024, row = (u / 16) % 64, k-chunk kc = u % 16
+  const uint16_t* X = (const uint16_t*)a.X;
+  const uint16_t* xsrc[8];
+  int sdst[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int u = threadIdx.x + 256 * i;
+    const int p = u >> 10, row = (u >> 4) & 63, kc = u & 15;
+    const int r = min(rbase + row, rend - 1);
+    xsrc[i] = X + (size_t)p * a.x_lo + (size_t)r * a.K + ks0 * 32 + kc * 8;
+    const int mt = row >> 4, ku = kc >> 2, ln = (row & 15) + 16 * (kc & 3);
+    sdst[i] = ((p * 4 + mt) * kRB_UK + ku) * kRB_FRAG + ln * 16;
+  }
+
+  f32x4_t acc[4][2];
+#pragma unroll
+  for (int m = 0; m < 4; ++m) { acc[m][0] = f32x4_t{0.f, 0.f, 0.f, 0.f}; acc[m][1] = acc[m][0]; }
+
+  uint4 stg[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) stg[i] = *(const uint4*)xsrc[i];
+  for (int kk = 0; kk < a.ksteps; kk += kRB_UK) {
+    __syncthreads();                                  // previous stage fully consumed
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *(uint4*)(sA + sdst[i]) = stg[i];
+    uint4 b[kRB_UK][2];
+#pragma unroll
+    for (int u = 0; u < kRB_UK; ++u) { b[u][0] = wp0[(kk + u) * 64]; b[u][1] = wp1[(kk + u) * 64]; }
+    __syncthreads();
+    if (kk + kRB_UK < a.ksteps) {                     // prefetch the next stage
+#pragma unroll
+      for (int i = 0; i < 8; ++i) stg[i] = *(const uint4*)(xsrc[i] + (kk + kRB_UK) * 32);
+    }
+#pragma unroll
+    for (int u = 0; u < kRB_UK; ++u) {
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        const uint4 ah = *(const uint4*)(sA + ((0 * 4 + m) * kRB_UK + u) * kRB_FRAG + lane * 16);
+        const uint4 al = *(const uint4*)(sA + ((1 * 4 + m) * kRB_UK + u) * kRB_FRAG + lane * 16);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ah),
+                                                              __builtin_bit_cast(bf16x8_t, b[u][j]), acc[m][j], 0, 0, 0);
+          acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, al),
+                                                              __builtin_bit_cast(bf16x8_t, b[u][j]), acc[m][j], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  const int col = lane & 15;
+  const int rq = (lane >> 4) * 4;
+  if (EPI == EPI_F32) {
+    float* out = a.out + (size_t)s * a.out_split;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = rbase + m * 16 + rq + i;
+          if (r < rend) out[(size_t)r * a.N + (nt0 + j) * 16 + col] = acc[m][j][i];
+        }
+  } else {
+    const int half = a.N >> 1;
+#pragma unroll
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = rbase + m * 16 + rq + i;
+        if (r < rend) {
+          const float g = acc[m][0][i], u = acc[m][1][i];
+          store_split(a.hout, a.h_lo, (size_t)r * half + (nt0 >> 1) * 16 + col, g / (1.f + __expf(-g)) * u);
+        }
+      }
+  }
+}
+
 // ------------------------------------------------------------ fp32 GEMM
 // Plain fp32 FMA GEMM for the fp32 engine mode: a workgroup computes 16 rows
 // x 64 columns; W is row-major [N][K].
@@ -289,19 +445,24 @@ __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ part,
                                                  const int* __restrict__ bt_store, const float2* __restrict__ tab,
                                                  float* __restrict__ qv, void* __restrict__ kvv, int layer, int NB,
                                                  int n_h, int n_kv, int hd) {
+  // work items of a row: (n_h + n_kv) * hd/2 rotation pairs, then n_kv * hd v elements
   const int t = blockIdx.x;
-  const int pos = row_pos[t];
+  const int item = blockIdx.y * 256 + threadIdx.x;
   const int half = hd >> 1;
+  const int npairs = (n_h + n_kv) * half;
+  if (item >= npairs + n_kv * hd) return;
+  const int pos = row_pos[t];
   const int qkv = (n_h + 2 * n_kv) * hd;
   const float* pr = part + (size_t)t * qkv;
   const int blk = bt_store[row_bt[t] + (pos >> 4)];
   const int off = pos & 15;
   const size_t hs = (size_t)2 * kBlock * hd;
   const size_t lbase = ((size_t)layer * NB + blk) * n_kv * hs;
-  for (int i = threadIdx.x; i < (n_h + n_kv) * half; i += 256) {
-    const int head = i / half, jj = i - head * half;
+  if (item < npairs) {
+    const int head = item / half, jj = item - head * half;
     const int c = head * hd + jj;
     float x1 = 0.f, x2 = 0.f;
+#pragma unroll 16
     for (int s = 0; s < nsplit; ++s) {
       x1 += pr[(size_t)s * split_stride + c];
       x2 += pr[(size_t)s * split_stride + c + half];
@@ -318,11 +479,12 @@ __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ part,
       if (BF) { ((uint16_t*)kvv)[o] = f2bf(y1); ((uint16_t*)kvv)[o + half] = f2bf(y2); }
       else { ((float*)kvv)[o] = y1; ((float*)kvv)[o + half] = y2; }
     }
-  }
-  for (int i = threadIdx.x; i < n_kv * hd; i += 256) {
+  } else {
+    const int i = item - npairs;
     const int kh = i / hd, dd = i - kh * hd;
     const int c = (n_h + n_kv) * hd + i;
     float v = 0.f;
+#pragma unroll 16
     for (int s = 0; s < nsplit; ++s) v += pr[(size_t)s * split_stride + c];
     const size_t o = lbase + (size_t)kh * hs + kBlock * hd + off * hd + dd;
     if (BF) ((uint16_t*)kvv)[o] = f2bf(v);
@@ -479,8 +641,10 @@ __global__ void k_attn_reduce(const ReduceItem* __restrict__ red, const float* _
   const int h = blockIdx.y;
   const int dd = threadIdx.x;
   float M = -INFINITY;
+#pragma unroll 8
   for (int s = 0; s < it.nslots; ++s) M = fmaxf(M, pml[((size_t)(it.slot0 + s) * n_h + h) * 2]);
   float L = 0.f, o = 0.f;
+#pragma unroll 8
   for (int s = 0; s < it.nslots; ++s) {
     const size_t b = (size_t)(it.slot0 + s) * n_h + h;
     const float wgt = exp2f(pml[b * 2] - M);
@@ -495,17 +659,22 @@ __global__ void k_attn_reduce(const ReduceItem* __restrict__ red, const float* _
 // ------------------------------------------------------------------ argmax
 // Greedy sampler: the largest fp32 logit, ties to the lowest token id; the
 // token is written into the device token store (it feeds the next step).
-__global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits, int V,
-                                                const int* __restrict__ lm_dst, int* __restrict__ tok) {
-  __shared__ float sv[4];
-  __shared__ int si[4];
+__global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logits, int V,
+                                                 const int* __restrict__ lm_dst, int* __restrict__ tok) {
+  __shared__ float sv[16];
+  __shared__ int si[16];
   const int r = blockIdx.x;
   const float* lr = logits + (size_t)r * V;
   float best = -INFINITY;
   int bi = INT_MAX;
-  for (int v = threadIdx.x; v < V; v += 256) {
-    const float x = lr[v];
-    if (x > best) { best = x; bi = v; }
+  // V % 4 == 0: each thread scans float4 groups in increasing index order, so a
+  // strict '>' keeps the lowest index among its equal maxima.
+  for (int v4 = threadIdx.x; v4 < V / 4; v4 += 1024) {
+    const float4 x = *(const float4*)(lr + 4 * v4);
+    if (x.x > best) { best = x.x; bi = 4 * v4; }
+    if (x.y > best) { best = x.y; bi = 4 * v4 + 1; }
+    if (x.z > best) { best = x.z; bi = 4 * v4 + 2; }
+    if (x.w > best) { best = x.w; bi = 4 * v4 + 3; }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -519,7 +688,7 @@ __global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits
   if (threadIdx.x == 0) {
     best = sv[0];
     bi = si[0];
-    for (int k = 1; k < 4; ++k)
+    for (int k = 1; k < 16; ++k)
       if (sv[k] > best || (sv[k] == best && si[k] < bi)) { best = sv[k]; bi = si[k]; }
     tok[lm_dst[r]] = (bi == INT_MAX) ? 0 : bi;
   }
@@ -530,8 +699,8 @@ __global__ __launch_bounds__(256) void k_argmax(const float* __restrict__ logits
 hipError_t launch_embed(hipStream_t st, bool bf16, const int* tok_store, const int* row_tok,
                         const int* row_model, ModelPtrs embed, float* x, int T, int d) {
   if (T <= 0) return hipSuccess;
-  if (bf16) k_embed<true><<<T, 256, 0, st>>>(tok_store, row_tok, row_model, embed, x, d);
-  else k_embed<false><<<T, 256, 0, st>>>(tok_store, row_tok, row_model, embed, x, d);
+  if (bf16) klaunch(k_embed<true>, dim3(T), dim3(256), st, tok_store, row_tok, row_model, embed, x, d);
+  else klaunch(k_embed<false>, dim3(T), dim3(256), st, tok_store, row_tok, row_model, embed, x, d);
   return hipGetLastError();
 }
 
@@ -539,19 +708,21 @@ hipError_t launch_add_rmsnorm(hipStream_t st, bool bf16, float* x, const float* 
                               size_t split_stride, const int* gather, const int* row_model, int nrows,
                               ModelPtrs gamma, void* out, size_t out_lo, int d, float eps) {
   if (nrows <= 0) return hipSuccess;
+  if (d % 256 || d > 4096) return hipErrorInvalidValue;   // one float4 per thread, <= 1024 threads
+  const int threads = d / 4;
   if (bf16)
-    k_add_rmsnorm<true><<<nrows, 256, 0, st>>>(x, part, nsplit, split_stride, gather, row_model, gamma, out, out_lo,
-                                               d, eps);
+    klaunch(k_add_rmsnorm<true>, dim3(nrows), dim3(threads), st, x, part, nsplit, split_stride, gather, row_model,
+            gamma, out, out_lo, d, eps);
   else
-    k_add_rmsnorm<false><<<nrows, 256, 0, st>>>(x, part, nsplit, split_stride, gather, row_model, gamma, out, out_lo,
-                                                d, eps);
+    klaunch(k_add_rmsnorm<false>, dim3(nrows), dim3(threads), st, x, part, nsplit, split_stride, gather, row_model,
+            gamma, out, out_lo, d, eps);
   return hipGetLastError();
 }
 
 template <int MT, int NT, int EPI>
 static void gemm_u(hipStream_t st, const GemmArgs& a, int blocks) {
-  if (a.ksteps % 8 == 0) k_gemm_bf16<MT, NT, EPI, 8><<<blocks, 256, 0, st>>>(a);
-  else k_gemm_bf16<MT, NT, EPI, 4><<<blocks, 256, 0, st>>>(a);
+  if (a.ksteps % 8 == 0) klaunch(k_gemm_bf16<MT, NT, EPI, 8>, dim3(blocks), dim3(256), st, a);
+  else klaunch(k_gemm_bf16<MT, NT, EPI, 4>, dim3(blocks), dim3(256), st, a);
 }
 
 template <int MT>
@@ -563,8 +734,15 @@ static void gemm_nt(hipStream_t st, const GemmArgs& a, int blocks, int epi, int 
 
 hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt) {
   if (a.total_items <= 0) return hipSuccess;
+  if (bf16 && mt == kRowBlock) {
+    const int nwg = a.total_items;
+    const int grid = (nwg + 7) / 8 * 8;
+    if (epi == EPI_SWIGLU) klaunch(k_gemm_bf16_rb<EPI_SWIGLU>, dim3(grid), dim3(256), st, a, nwg);
+    else klaunch(k_gemm_bf16_rb<EPI_F32>, dim3(grid), dim3(256), st, a, nwg);
+    return hipGetLastError();
+  }
   if (!bf16) {
-    k_gemm_f32<<<a.total_items, 256, 0, st>>>(a);
+    klaunch(k_gemm_f32, dim3(a.total_items), dim3(256), st, a);
     return hipGetLastError();
   }
   const int blocks = (a.total_items + 3) / 4;
@@ -576,7 +754,7 @@ hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, in
 
 hipError_t launch_swiglu_f32(hipStream_t st, const float* gu, float* h, int T, int ffn) {
   if (T <= 0) return hipSuccess;
-  k_swiglu_f32<<<T, 256, 0, st>>>(gu, h, ffn);
+  klaunch(k_swiglu_f32, dim3(T), dim3(256), st, gu, h, ffn);
   return hipGetLastError();
 }
 
@@ -585,11 +763,13 @@ hipError_t launch_rope_kv(hipStream_t st, bool bf16, const float* part, int nspl
                           const float2* rope_tab, float* q, void* kv, int layer, int num_blocks,
                           int n_h, int n_kv, int hd, int T) {
   if (T <= 0) return hipSuccess;
+  const int items = (n_h + n_kv) * (hd / 2) + n_kv * hd;
+  const dim3 grid(T, (items + 255) / 256);
   if (bf16)
-    k_rope_kv<true><<<T, 256, 0, st>>>(part, nsplit, split_stride, row_pos, row_bt, bt_store, rope_tab, q, kv,
+    klaunch(k_rope_kv<true>, grid, dim3(256), st, part, nsplit, split_stride, row_pos, row_bt, bt_store, rope_tab, q, kv,
                                        layer, num_blocks, n_h, n_kv, hd);
   else
-    k_rope_kv<false><<<T, 256, 0, st>>>(part, nsplit, split_stride, row_pos, row_bt, bt_store, rope_tab, q, kv,
+    klaunch(k_rope_kv<false>, grid, dim3(256), st, part, nsplit, split_stride, row_pos, row_bt, bt_store, rope_tab, q, kv,
                                         layer, num_blocks, n_h, n_kv, hd);
   return hipGetLastError();
 }
@@ -599,10 +779,10 @@ static hipError_t attn_gq(hipStream_t st, int gq, dim3 grid, const AttnItem* ite
                           const int* bt, const int* row_bt, int layer, int NB, int n_h, int n_kv, float sl2,
                           void* out, size_t out_lo, float* pacc, float* pml) {
   switch (gq) {
-    case 1: k_attn<HD, 1, BF><<<grid, 64, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 2: k_attn<HD, 2, BF><<<grid, 128, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 4: k_attn<HD, 4, BF><<<grid, 256, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 8: k_attn<HD, 8, BF><<<grid, 512, 0, st>>>(items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 1: klaunch(k_attn<HD, 1, BF>, dim3(grid), dim3(64), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 2: klaunch(k_attn<HD, 2, BF>, dim3(grid), dim3(128), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 4: klaunch(k_attn<HD, 4, BF>, dim3(grid), dim3(256), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 8: klaunch(k_attn<HD, 8, BF>, dim3(grid), dim3(512), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -632,14 +812,15 @@ hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, 
                               int hd) {
   if (nred <= 0) return hipSuccess;
   dim3 grid(nred, n_h);
-  if (bf16) k_attn_reduce<true><<<grid, hd, 0, st>>>(red, pacc, pml, out, out_lo, n_h, hd);
-  else k_attn_reduce<false><<<grid, hd, 0, st>>>(red, pacc, pml, out, out_lo, n_h, hd);
+  if (bf16) klaunch(k_attn_reduce<true>, dim3(grid), dim3(hd), st, red, pacc, pml, out, out_lo, n_h, hd);
+  else klaunch(k_attn_reduce<false>, dim3(grid), dim3(hd), st, red, pacc, pml, out, out_lo, n_h, hd);
   return hipGetLastError();
 }
 
 hipError_t launch_argmax(hipStream_t st, const float* logits, int R, int V, const int* lm_dst, int* tok_store) {
   if (R <= 0) return hipSuccess;
-  k_argmax<<<R, 256, 0, st>>>(logits, V, lm_dst, tok_store);
+  if (V % 4) return hipErrorInvalidValue;
+  klaunch(k_argmax, dim3(R), dim3(1024), st, logits, V, lm_dst, tok_store);
   return hipGetLastError();
 }
 

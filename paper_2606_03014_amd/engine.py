@@ -74,6 +74,12 @@ class Engine:
     def chunks(self, rid):
         return M.moa_debug_chunks(self.h, rid)
 
+    def time_kernels(self, every, peak_bw=8.0e12, peak_flops=2.5e15):
+        M.moa_debug_time_kernels(self.h, every, peak_bw, peak_flops)
+
+    def kernel_stats(self):
+        return M.moa_debug_kernel_stats(self.h)
+
     def capture_logits(self, rid, arr):
         M.moa_debug_capture_logits(self.h, rid, arr)
 

@@ -48,6 +48,15 @@ class moa_request_info(C.Structure):
                 ("n_chunks", C.c_int32), ("state", C.c_int32)]
 
 
+class moa_kernel_stats(C.Structure):
+    _fields_ = [("launches", C.c_int64), ("ms", C.c_double), ("bytes", C.c_double), ("flops", C.c_double),
+                ("launches_all", C.c_int64), ("bytes_all", C.c_double), ("flops_all", C.c_double),
+                ("roof_ms_all", C.c_double)]
+
+
+KERNEL_CLASSES = ["embed", "norm", "gemm_qkv", "rope_kv", "attn", "attn_reduce", "gemm_o",
+                  "gemm_gateup", "gemm_down", "gemm_lmhead", "argmax"]
+
 P = C.POINTER
 _SIGS = {
     "moa_arena_bytes": (C.c_int, [P(moa_engine_cfg), P(C.c_size_t)]),
@@ -65,6 +74,8 @@ _SIGS = {
     "moa_debug_chunks": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_int64), C.c_int32, P(C.c_int32)]),
     "moa_debug_steps": (C.c_int, [C.c_void_p, P(C.c_int64), C.c_int64, P(C.c_int64)]),
     "moa_debug_capture_logits": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_float)]),
+    "moa_debug_time_kernels": (C.c_int, [C.c_void_p, C.c_int32, C.c_double, C.c_double]),
+    "moa_debug_kernel_stats": (C.c_int, [C.c_void_p, P(moa_kernel_stats)]),
 }
 
 _lib = None
@@ -220,3 +231,15 @@ def moa_debug_capture_logits(eng, rid, host_array):
     """host_array: float32 numpy array of max_new_tokens * vocab, kept alive by the caller."""
     check(lib().moa_debug_capture_logits(eng, rid, host_array.ctypes.data_as(P(C.c_float))),
           "moa_debug_capture_logits")
+
+
+def moa_debug_time_kernels(eng, every, peak_bw=8.0e12, peak_flops=2.5e15):
+    check(lib().moa_debug_time_kernels(eng, every, peak_bw, peak_flops), "moa_debug_time_kernels")
+
+
+def moa_debug_kernel_stats(eng):
+    """{class name: dict of the moa_kernel_stats fields}."""
+    out = (moa_kernel_stats * len(KERNEL_CLASSES))()
+    check(lib().moa_debug_kernel_stats(eng, out), "moa_debug_kernel_stats")
+    return {n: {f: getattr(out[i], f) for f, _ in moa_kernel_stats._fields_}
+            for i, n in enumerate(KERNEL_CLASSES)}

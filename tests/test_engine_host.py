@@ -15,7 +15,7 @@ from paper_2606_03014_amd import moa as M
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 GOLD = json.load(open(os.path.join(ROOT, "tests", "golden", "step_rule_examples.json")))
-TOY = ModelShape(1, 128, 2, 2, 64, 128, 256)
+TOY = ModelShape(1, 256, 4, 2, 64, 256, 256)
 
 
 def _blob_bytes(shape, dtype):
