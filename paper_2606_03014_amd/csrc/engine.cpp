@@ -358,16 +358,18 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     return;
   }
   const int KS = K / 32;
-  const bool row_block = maxM > 32 && N % 128 == 0;
+  const int wmt = maxM <= 16 ? 1 : (maxM <= 32 ? 2 : 4);
+  const int wnt = (maxM > 64 && N % 256 == 0) ? 4 : 2;
+  const bool wg = N % (64 * wnt) == 0;
   int tiles, rows_per, target, base = 0;
-  if (row_block) {          // workgroup items: 64 rows x 128 columns
-    mt = kRowBlock;
-    nt = 2;
-    tiles = N / 128;
-    rows_per = 64;
+  if (wg) {                 // workgroup items: 16*wmt rows x 64*wnt columns
+    mt = kWgTile + wmt;
+    nt = wnt;
+    tiles = N / (64 * wnt);
+    rows_per = 16 * wmt;
     target = kTargetWaves / 4;
   } else {                  // wavefront items: 16*mt rows x 16*nt columns
-    mt = maxM <= 16 ? 1 : (maxM <= 32 ? 2 : 4);
+    mt = wmt;
     nt = (epi == EPI_SWIGLU) ? 2 : 1;
     tiles = N / 16 / nt;
     rows_per = 16 * mt;
@@ -744,7 +746,11 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
     flops = 2.0 * rows * a.N * a.K;
   };
   double kv_keys = 0;
-  for (const AttnItem& it : e->items) kv_keys += it.k1 - it.k0;
+  int max_item_blocks = 1;
+  for (const AttnItem& it : e->items) {
+    kv_keys += it.k1 - it.k0;
+    max_item_blocks = std::max(max_item_blocks, ((it.k1 - 1) >> 4) - (it.k0 >> 4) + 1);
+  }
   const double attn_bytes = kv_keys * nkv * 2.0 * hd * esz + (double)T * nh * hd * 8.0;
   const double attn_flops = kv_keys * nh * hd * 4.0;
   const double norm_bytes = (double)T * d * 12.0;
@@ -771,7 +777,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
              launch_rope_kv(s, bf, e->part, ga.S, ga.out_split, sd.row_pos, sd.row_bt, e->bt_store, e->rope, e->q,
                             e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd, T), "rope kv");
       LAUNCH(MOA_K_ATTN, attn_bytes, attn_flops,
-             launch_attention(s, bf, sd.items, nitems, e->q, e->kv, e->bt_store, sd.row_bt, l,
+             launch_attention(s, bf, sd.items, nitems, max_item_blocks, e->q, e->kv, e->bt_store, sd.row_bt, l,
                               e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc,
                               e->pml), "attention");
       if (nred > 0)

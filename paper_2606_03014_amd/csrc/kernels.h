@@ -40,9 +40,9 @@ struct GemmArgs {
 
 enum Epilogue { EPI_F32 = 0, EPI_SWIGLU = 1 };
 
-// launch_gemm(mt = kRowBlock): the LDS row-block kernel; each GemmArgs item is
-// one workgroup of 64 rows x 128 columns x one k-split (N % 128 == 0).
-constexpr int kRowBlock = 64;
+// launch_gemm(mt = kWgTile + MT, nt = NT): the workgroup-tile kernel; each item
+// is one workgroup of 16*MT rows x 64*NT columns x one k-split (N % (64*NT) == 0).
+constexpr int kWgTile = 1000;
 
 // Attention work item: one query row against keys [k0, k1) of its request.
 struct AttnItem { int row, k0, k1, slot; };   // slot < 0: write the final output
@@ -80,7 +80,8 @@ hipError_t launch_rope_kv(hipStream_t st, bool bf16, const float* part, int nspl
                           const float2* rope_tab, float* q, void* kv, int layer, int num_blocks,
                           int n_h, int n_kv, int hd, int T);
 
-hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, int nitems,
+// max_item_blocks: the most KV blocks any item's key range touches (LDS list).
+hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, int nitems, int max_item_blocks,
                             const float* q, const void* kv, const int* bt_store, const int* row_bt,
                             int layer, int num_blocks, int n_h, int n_kv, int hd, float scale,
                             void* out, size_t out_lo, float* pacc, float* pml);

@@ -25,15 +25,22 @@ void set_launch_events(hipEvent_t start, hipEvent_t stop) {
 }
 
 template <typename... KArgs, typename... Args>
-static void klaunch(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t st, Args... args) {
+static void klaunch_shm(void (*kernel)(KArgs...), dim3 grid, dim3 block, unsigned shm, hipStream_t st,
+                        Args... args) {
   if (g_ev_start)
-    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, g_ev_start, g_ev_stop, 0, args...);
+    hipExtLaunchKernelGGL(kernel, grid, block, shm, st, g_ev_start, g_ev_stop, 0, args...);
   else
-    kernel<<<grid, block, 0, st>>>(args...);
+    kernel<<<grid, block, shm, st>>>(args...);
+}
+
+template <typename... KArgs, typename... Args>
+static void klaunch(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t st, Args... args) {
+  klaunch_shm(kernel, grid, block, 0u, st, args...);
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
@@ -266,24 +273,22 @@ __global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs a) {
   }
 }
 
-// ------------------------------------------- bf16 GEMM, row-block variant
-// For groups with more than 32 rows. A workgroup (4 wavefronts) owns 64 rows
-// x 128 columns x one k-split: the split-bf16 activation block (64 rows, both
-// planes) is staged once per 128-wide k stage in LDS, laid out in MFMA
-// A-fragment order (one 1 KB lane-ordered fragment per 16 rows x 32 k x plane,
-// so fragment reads are contiguous), and each wavefront streams its own two
-// 16-column weight tiles from HBM. Activation traffic is thus paid per
-// workgroup instead of per wavefront. Workgroup ids are remapped so that
-// consecutive logical blocks -- the row chunks that share weight tiles -- run
-// on the same XCD and share its L2.
-constexpr int kRB_UK = 4;                       // k-steps (of 32) per LDS stage
-constexpr int kRB_FRAG = 64 * 16;               // bytes per fragment
-constexpr int kRB_STAGE = 2 * 4 * kRB_UK * kRB_FRAG;   // planes x m-tiles x k-steps
-
-template <int EPI>
-__global__ __launch_bounds__(256) void k_gemm_bf16_rb(GemmArgs a, int nwg) {
-  __shared__ __align__(16) unsigned char sA[kRB_STAGE];
-  // XCD-aware remap: physical workgroup p runs on XCD p % 8
+// --------------------------------------- bf16 GEMM, workgroup-tile variant
+// A workgroup (4 wavefronts) owns 16*MT rows x 64*NT columns x one k-split.
+// Per stage of 4 MFMA k-steps (128 k) the split-bf16 activation block (both
+// planes) is staged in LDS in MFMA A-fragment order (1 KB lane-ordered
+// fragments, so every LDS read and write is contiguous) and shared by the four
+// wavefronts; each wavefront streams its own NT weight tiles of 16 columns
+// from HBM. LDS is double-buffered with one barrier per stage, and the next
+// stage's activation and weight loads are issued before the current stage's
+// MFMAs, so HBM latency overlaps compute. Workgroup ids are remapped so that
+// the row blocks sharing weight tiles run on the same XCD (shared L2).
+template <int MT, int NT, int EPI>
+__global__ __launch_bounds__(256) void k_gemm_wg(GemmArgs a, int nwg) {
+  constexpr int UK = 4;                              // k-steps per stage
+  constexpr int UNITS = 2 * MT * UK * 64;            // 16-byte units per stage (both planes)
+  constexpr int PER = UNITS / 256;                   // per thread
+  __shared__ __align__(16) unsigned char sA[2][UNITS * 16];
   const int per = (nwg + 7) / 8;
   const int blk = (blockIdx.x % 8) * per + blockIdx.x / 8;
   if (blk >= a.total_items) return;
@@ -302,63 +307,86 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_rb(GemmArgs a, int nwg) {
   const int s = rest % a.S;
   const int nb = rest / a.S;
   const int ks0 = s * a.ksteps;
-  const int nt0 = nb * 8 + w * 2;             // this wavefront's two 16-column tiles
+  const int nt0 = (nb * 4 + w) * NT;                 // this wavefront's first 16-column tile
   const int KS = a.K >> 5;
-  const uint4* W = (const uint4*)Wg;
-  const uint4* wp0 = W + ((size_t)nt0 * KS + ks0) * 64 + lane;
-  const uint4* wp1 = W + ((size_t)(nt0 + 1) * KS + ks0) * 64 + lane;
-  const int rbase = row0 + mc * 64;
+  const u32x4* wp = (const u32x4*)Wg + ((size_t)nt0 * KS + ks0) * 64 + lane;
+  const size_t wt = (size_t)KS * 64;                 // u32x4 distance between tiles
+  const int rbase = row0 + mc * MT * 16;
   const int rend = row0 + nrows;
 
-  // staging map: thread t moves 16-byte units u = t + 256*i (i < 8) of the
-  // stage: plane p = u / 1024, row = (u / 16) % 64, k-chunk kc = u % 16
+  // Staging: unit u = t + 256*i is lane ln = u % 64 of fragment (plane p,
+  // m-tile mt, k-step ku) = (u / (MT*UK*64), (u / (UK*64)) % MT, (u / 64) % UK):
+  // row 16*mt + ln % 16, k = 32*ku + 8*(ln / 16) .. +8 of that plane.
   const uint16_t* X = (const uint16_t*)a.X;
-  const uint16_t* xsrc[8];
-  int sdst[8];
+  size_t xoff[PER];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < PER; ++i) {
     const int u = threadIdx.x + 256 * i;
-    const int p = u >> 10, row = (u >> 4) & 63, kc = u & 15;
-    const int r = min(rbase + row, rend - 1);
-    xsrc[i] = X + (size_t)p * a.x_lo + (size_t)r * a.K + ks0 * 32 + kc * 8;
-    const int mt = row >> 4, ku = kc >> 2, ln = (row & 15) + 16 * (kc & 3);
-    sdst[i] = ((p * 4 + mt) * kRB_UK + ku) * kRB_FRAG + ln * 16;
+    const int ln = u & 63, ku = (u >> 6) % UK, mt = (u / (UK * 64)) % MT, p = u / (MT * UK * 64);
+    const int r = min(rbase + mt * 16 + (ln & 15), rend - 1);
+    xoff[i] = (size_t)p * a.x_lo + (size_t)r * a.K + (size_t)ks0 * 32 + ku * 32 + (ln >> 4) * 8;
   }
 
-  f32x4_t acc[4][2];
+  f32x4_t acc[MT][NT];
 #pragma unroll
-  for (int m = 0; m < 4; ++m) { acc[m][0] = f32x4_t{0.f, 0.f, 0.f, 0.f}; acc[m][1] = acc[m][0]; }
+  for (int m = 0; m < MT; ++m)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[m][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  uint4 stg[8];
+  u32x4 stg[PER], b[UK][NT];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) stg[i] = *(const uint4*)xsrc[i];
-  for (int kk = 0; kk < a.ksteps; kk += kRB_UK) {
-    __syncthreads();                                  // previous stage fully consumed
+  for (int i = 0; i < PER; ++i) stg[i] = *(const u32x4*)(X + xoff[i]);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) *(uint4*)(sA + sdst[i]) = stg[i];
-    uint4 b[kRB_UK][2];
+  for (int u = 0; u < UK; ++u)
 #pragma unroll
-    for (int u = 0; u < kRB_UK; ++u) { b[u][0] = wp0[(kk + u) * 64]; b[u][1] = wp1[(kk + u) * 64]; }
-    __syncthreads();
-    if (kk + kRB_UK < a.ksteps) {                     // prefetch the next stage
+    for (int j = 0; j < NT; ++j) b[u][j] = wp[j * wt + u * 64];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) stg[i] = *(const uint4*)(xsrc[i] + (kk + kRB_UK) * 32);
+  for (int i = 0; i < PER; ++i) *(u32x4*)(sA[0] + (threadIdx.x + 256 * i) * 16) = stg[i];
+  __syncthreads();
+
+  const int nstage = a.ksteps / UK;
+  for (int st = 0; st < nstage; ++st) {
+    const int cur = st & 1;
+    const bool more = st + 1 < nstage;
+    u32x4 bn[UK][NT];
+    if (more) {                                       // next stage: activations and weights
+      const size_t ko = (size_t)(st + 1) * UK * 32;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) stg[i] = *(const u32x4*)(X + xoff[i] + ko);
+#pragma unroll
+      for (int u = 0; u < UK; ++u)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) bn[u][j] = wp[j * wt + ((st + 1) * UK + u) * 64];
     }
+    const unsigned char* A = sA[cur];
 #pragma unroll
-    for (int u = 0; u < kRB_UK; ++u) {
+    for (int u = 0; u < UK; ++u) {
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const uint4 ah = *(const uint4*)(sA + ((0 * 4 + m) * kRB_UK + u) * kRB_FRAG + lane * 16);
-        const uint4 al = *(const uint4*)(sA + ((1 * 4 + m) * kRB_UK + u) * kRB_FRAG + lane * 16);
+      for (int m = 0; m < MT; ++m) {
+        const u32x4 ah = *(const u32x4*)(A + ((0 * MT + m) * UK + u) * 1024 + lane * 16);
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < NT; ++j)
           acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ah),
                                                               __builtin_bit_cast(bf16x8_t, b[u][j]), acc[m][j], 0, 0, 0);
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        const u32x4 al = *(const u32x4*)(A + ((1 * MT + m) * UK + u) * 1024 + lane * 16);
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
           acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, al),
                                                               __builtin_bit_cast(bf16x8_t, b[u][j]), acc[m][j], 0, 0, 0);
-        }
       }
     }
+    if (more) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) *(u32x4*)(sA[cur ^ 1] + (threadIdx.x + 256 * i) * 16) = stg[i];
+#pragma unroll
+      for (int u = 0; u < UK; ++u)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) b[u][j] = bn[u][j];
+    }
+    __syncthreads();
   }
 
   const int col = lane & 15;
@@ -366,9 +394,9 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_rb(GemmArgs a, int nwg) {
   if (EPI == EPI_F32) {
     float* out = a.out + (size_t)s * a.out_split;
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < MT; ++m)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NT; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int r = rbase + m * 16 + rq + i;
@@ -377,15 +405,17 @@ __global__ __launch_bounds__(256) void k_gemm_bf16_rb(GemmArgs a, int nwg) {
   } else {
     const int half = a.N >> 1;
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+    for (int m = 0; m < MT; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = rbase + m * 16 + rq + i;
-        if (r < rend) {
-          const float g = acc[m][0][i], u = acc[m][1][i];
-          store_split(a.hout, a.h_lo, (size_t)r * half + (nt0 >> 1) * 16 + col, g / (1.f + __expf(-g)) * u);
+      for (int p = 0; p < NT / 2; ++p)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = rbase + m * 16 + rq + i;
+          if (r < rend) {
+            const float g = acc[m][2 * p][i], u = acc[m][2 * p + 1][i];
+            store_split(a.hout, a.h_lo, (size_t)r * half + ((nt0 >> 1) + p) * 16 + col, g / (1.f + __expf(-g)) * u);
+          }
         }
-      }
   }
 }
 
@@ -495,13 +525,16 @@ __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ part,
 // ------------------------------------------------ paged attention (split-KV)
 // One workgroup = one query row x one KV head x one key range [k0, k1); its
 // GQ wavefronts are the GQ query heads that share the KV head, so each K/V
-// tile is read from HBM once for the whole group. Tiles of 64 keys are
-// staged in LDS with 16-byte coalesced loads (a 16-slot block of one KV head
-// is contiguous). In a tile, lane l owns key 8*p + l/8 (p = 0..7) and head-dim
-// chunk l%8: q.k partial dots are combined across the 8 lanes of a key with
-// xor-shuffles, the tile max across the wavefront with shuffles, and P.V
-// accumulates per lane on its own keys and dims (combined once at the end).
-// Softmax runs in base 2 on scores pre-scaled by log2(e)/sqrt(hd).
+// tile is read from HBM once for the whole group. The range's block ids are
+// first copied to LDS (dynamic shared memory sized by the host), then tiles
+// of 64 keys are staged in LDS with 16-byte coalesced loads (a 16-slot block
+// of one KV head is contiguous); the next tile's loads are issued into
+// registers before the current tile is computed. In a tile, lane l owns key
+// 8*p + l/8 (p = 0..7) and head-dim chunk l%8: q.k partial dots are combined
+// across the 8 lanes of a key with xor-shuffles, the tile max across the
+// wavefront with shuffles, and P.V accumulates per lane on its own keys and
+// dims (combined once at the end). Softmax runs in base 2 on scores
+// pre-scaled by log2(e)/sqrt(hd).
 template <int HD, int GQ, bool BF>
 __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ items, const float* __restrict__ qv,
                                                   const void* __restrict__ kvv, const int* __restrict__ bt_store,
@@ -512,10 +545,13 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
   constexpr int CH = HD / 8;
   constexpr int ESZ = BF ? 2 : 4;
   constexpr int ROWB = HD * ESZ;
-  constexpr int CPR = ROWB / 16;
-  constexpr int NCH = 2 * TK * CPR;
+  constexpr int CPR = ROWB / 16;                 // 16-byte chunks per key row
+  constexpr int NCH = 2 * TK * CPR;              // chunks per tile (K and V)
+  constexpr int NT = GQ * 64;
+  constexpr int PER = (NCH + NT - 1) / NT;       // chunks per thread
   __shared__ __align__(16) unsigned char sK[TK * ROWB];
   __shared__ __align__(16) unsigned char sV[TK * ROWB];
+  extern __shared__ int sbt[];                   // block ids of the key range
 
   const AttnItem it = items[blockIdx.x];
   const int kvh = blockIdx.y;
@@ -523,6 +559,11 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
   const int g8 = lane >> 3, c8 = lane & 7;
   const int h = kvh * GQ + w;
 
+  const int b0 = it.k0 >> 4, nb = ((it.k1 - 1) >> 4) - b0 + 1;
+  {
+    const int* bt = bt_store + row_bt[it.row] + b0;
+    for (int i = threadIdx.x; i < nb; i += NT) sbt[i] = bt[i];
+  }
   float q[CH];
   {
     const size_t qo = ((size_t)it.row * n_h + h) * HD + c8 * CH;
@@ -532,27 +573,44 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
   float m = -INFINITY, l = 0.f, acc[CH];
 #pragma unroll
   for (int i = 0; i < CH; ++i) acc[i] = 0.f;
+  __syncthreads();
 
-  const int* bt = bt_store + row_bt[it.row];
-  const size_t hs = (size_t)2 * kBlock * HD;          // elements per (block, kv head)
-  const unsigned char* pool = (const unsigned char*)kvv;
-  const size_t layer_base = (size_t)layer * NB;
+  const size_t hs = (size_t)2 * kBlock * HD;     // elements per (block, kv head)
+  const unsigned char* pool = (const unsigned char*)kvv + ((size_t)layer * NB * n_kv + kvh) * hs * ESZ;
+  const size_t blk_stride = (size_t)n_kv * hs * ESZ;
 
-  for (int t0 = it.k0; t0 < it.k1; t0 += TK) {
-    for (int c = threadIdx.x; c < NCH; c += GQ * 64) {
-      const int isV = c / (TK * CPR);
-      const int rem = c - isV * (TK * CPR);
-      const int key = rem / CPR, cc = rem - key * CPR;
-      const int p = t0 + key;
+  uint4 pre[PER];
+  auto fetch = [&](int t0) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = threadIdx.x + j * NT;
       uint4 val = make_uint4(0u, 0u, 0u, 0u);
-      if (p < it.k1) {
-        const int blk = bt[p >> 4];
-        const size_t e = ((layer_base + blk) * n_kv + kvh) * hs + (size_t)isV * kBlock * HD + (size_t)(p & 15) * HD;
-        val = *(const uint4*)(pool + e * ESZ + cc * 16);
+      if (c < NCH) {
+        const int isV = c / (TK * CPR);
+        const int rem = c - isV * (TK * CPR);
+        const int key = rem / CPR, cc = rem - key * CPR;
+        const int p = t0 + key;
+        if (p < it.k1) {
+          const int blk = sbt[(p >> 4) - b0];
+          val = *(const uint4*)(pool + blk * blk_stride + ((size_t)isV * kBlock * HD + (p & 15) * HD) * ESZ + cc * 16);
+        }
       }
-      *(uint4*)((isV ? sV : sK) + key * ROWB + cc * 16) = val;
+      pre[j] = val;
+    }
+  };
+  fetch(it.k0);
+  for (int t0 = it.k0; t0 < it.k1; t0 += TK) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = threadIdx.x + j * NT;
+      if (c < NCH) {
+        const int isV = c / (TK * CPR);
+        const int rem = c - isV * (TK * CPR);
+        *(uint4*)((isV ? sV : sK) + rem * 16) = pre[j];
+      }
     }
     __syncthreads();
+    if (t0 + TK < it.k1) fetch(t0 + TK);
 
     float s[8];
 #pragma unroll
@@ -734,11 +792,21 @@ static void gemm_nt(hipStream_t st, const GemmArgs& a, int blocks, int epi, int 
 
 hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt) {
   if (a.total_items <= 0) return hipSuccess;
-  if (bf16 && mt == kRowBlock) {
+  if (bf16 && mt >= kWgTile) {
+    const int m = mt - kWgTile;          // rows / 16
     const int nwg = a.total_items;
     const int grid = (nwg + 7) / 8 * 8;
-    if (epi == EPI_SWIGLU) klaunch(k_gemm_bf16_rb<EPI_SWIGLU>, dim3(grid), dim3(256), st, a, nwg);
-    else klaunch(k_gemm_bf16_rb<EPI_F32>, dim3(grid), dim3(256), st, a, nwg);
+    const dim3 g(grid), b(256);
+#define WGL(M_, N_, E_) klaunch(k_gemm_wg<M_, N_, E_>, g, b, st, a, nwg)
+    if (epi == EPI_SWIGLU) {
+      if (nt == 4) { if (m == 1) WGL(1, 4, EPI_SWIGLU); else if (m == 2) WGL(2, 4, EPI_SWIGLU); else WGL(4, 4, EPI_SWIGLU); }
+      else { if (m == 1) WGL(1, 2, EPI_SWIGLU); else if (m == 2) WGL(2, 2, EPI_SWIGLU); else WGL(4, 2, EPI_SWIGLU); }
+    } else {
+      if (nt == 4) { if (m == 1) WGL(1, 4, EPI_F32); else if (m == 2) WGL(2, 4, EPI_F32); else WGL(4, 4, EPI_F32); }
+      else if (nt == 2) { if (m == 1) WGL(1, 2, EPI_F32); else if (m == 2) WGL(2, 2, EPI_F32); else WGL(4, 2, EPI_F32); }
+      else { if (m == 1) WGL(1, 1, EPI_F32); else if (m == 2) WGL(2, 1, EPI_F32); else WGL(4, 1, EPI_F32); }
+    }
+#undef WGL
     return hipGetLastError();
   }
   if (!bf16) {
@@ -775,34 +843,36 @@ hipError_t launch_rope_kv(hipStream_t st, bool bf16, const float* part, int nspl
 }
 
 template <int HD, bool BF>
-static hipError_t attn_gq(hipStream_t st, int gq, dim3 grid, const AttnItem* items, const float* q, const void* kv,
-                          const int* bt, const int* row_bt, int layer, int NB, int n_h, int n_kv, float sl2,
-                          void* out, size_t out_lo, float* pacc, float* pml) {
+static hipError_t attn_gq(hipStream_t st, int gq, dim3 grid, unsigned shm, const AttnItem* items, const float* q,
+                          const void* kv, const int* bt, const int* row_bt, int layer, int NB, int n_h, int n_kv,
+                          float sl2, void* out, size_t out_lo, float* pacc, float* pml) {
   switch (gq) {
-    case 1: klaunch(k_attn<HD, 1, BF>, dim3(grid), dim3(64), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 2: klaunch(k_attn<HD, 2, BF>, dim3(grid), dim3(128), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 4: klaunch(k_attn<HD, 4, BF>, dim3(grid), dim3(256), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 8: klaunch(k_attn<HD, 8, BF>, dim3(grid), dim3(512), st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 1: klaunch_shm(k_attn<HD, 1, BF>, grid, dim3(64), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 2: klaunch_shm(k_attn<HD, 2, BF>, grid, dim3(128), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 4: klaunch_shm(k_attn<HD, 4, BF>, grid, dim3(256), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 8: klaunch_shm(k_attn<HD, 8, BF>, grid, dim3(512), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, int nitems,
+hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, int nitems, int max_item_blocks,
                             const float* q, const void* kv, const int* bt_store, const int* row_bt,
                             int layer, int num_blocks, int n_h, int n_kv, int hd, float scale,
                             void* out, size_t out_lo, float* pacc, float* pml) {
   if (nitems <= 0) return hipSuccess;
+  const unsigned shm = (unsigned)max_item_blocks * 4u;
+  if (shm > 48u * 1024u) return hipErrorInvalidValue;
   const int gq = n_h / n_kv;
   const float sl2 = scale * 1.4426950408889634f;
   dim3 grid(nitems, n_kv);
   if (hd == 64) {
-    return bf16 ? attn_gq<64, true>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml)
-                : attn_gq<64, false>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
+    return bf16 ? attn_gq<64, true>(st, gq, grid, shm, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml)
+                : attn_gq<64, false>(st, gq, grid, shm, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
   }
   if (hd == 128) {
-    return bf16 ? attn_gq<128, true>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml)
-                : attn_gq<128, false>(st, gq, grid, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
+    return bf16 ? attn_gq<128, true>(st, gq, grid, shm, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml)
+                : attn_gq<128, false>(st, gq, grid, shm, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
   }
   return hipErrorInvalidValue;
 }
