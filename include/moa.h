@@ -195,14 +195,17 @@ moa_status moa_debug_capture_logits(moa_engine* e, int64_t request_id, float* ho
 /* Kernel classes of one step (for moa_debug_time_kernels). */
 enum {
   MOA_K_EMBED = 0, MOA_K_NORM, MOA_K_GEMM_QKV, MOA_K_ROPE_KV, MOA_K_ATTN, MOA_K_ATTN_REDUCE,
-  MOA_K_GEMM_O, MOA_K_GEMM_GATEUP, MOA_K_GEMM_DOWN, MOA_K_GEMM_LMHEAD, MOA_K_ARGMAX, MOA_K_COUNT
+  MOA_K_GEMM_O, MOA_K_GEMM_GATEUP, MOA_K_GEMM_DOWN, MOA_K_GEMM_LMHEAD, MOA_K_ARGMAX, MOA_K_PREFILL_ATTN,
+  MOA_K_COUNT
 };
 
 /* Per-class launch statistics of the sampled steps. bytes/flops are the
  * algorithmic figures of those launches: for a GEMM the bf16 weights it
  * streams (N*K*2 per model group) plus its split-bf16 input (M*K*4) and fp32
  * output (M*N*4), flops 2*M*N*K; for attention the bf16 K/V it reads
- * (keys*2*head_dim*2 per KV head) plus q (fp32) and its output. */
+ * (keys*2*head_dim*2 per KV head) plus q (fp32) and its output; for causal
+ * prefill attention each block's keys once per KV head, and 4*head_dim flops
+ * per (query head, query, visible key). */
 typedef struct {
   int64_t launches;   /* timed launches (sampled steps) */
   double ms;          /* their summed durations (HIP events on the engine's stream) */

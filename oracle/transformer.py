@@ -180,7 +180,8 @@ def forward_chunk(model, tokens, start, kv, bf16_kv=False, want="all"):
     """Run positions [start, start + len(tokens)) through the model, appending
     their K/V to ``kv`` (whose first ``start`` positions must already hold the
     history). Each position attends causally to positions <= itself.
-    Returns logits [len(tokens), vocab] (``want="last"``: only the last row)."""
+    Returns logits [len(tokens), vocab]; ``want="last"`` returns only the last
+    row, an integer ``want=j`` only rows j.. (the others are not computed)."""
     m = model.shape
     n_h, n_kv, hd = m.n_heads, m.n_kv_heads, m.head_dim
     store = bf16_round if bf16_kv else (lambda a: a)
@@ -213,14 +214,16 @@ def forward_chunk(model, tokens, start, kv, bf16_kv=False, want="all"):
         x = h + a @ model.W(p + "w_down").T
     if want == "last":
         x = x[-1:]
+    elif not isinstance(want, str):
+        x = x[want:]
     xf = rmsnorm(x, model.W("final_norm"), m.rms_eps)
     return xf @ model.W("lm_head").T
 
 
-def forward_full(model, tokens, bf16_kv=False):
-    """Logits at every position of ``tokens`` computed from scratch (no prior cache)."""
+def forward_full(model, tokens, bf16_kv=False, first=0):
+    """Logits at positions first.. of ``tokens`` computed from scratch (no prior cache)."""
     kv = ContiguousKV(model.n_layers, model.shape.n_kv_heads, model.shape.head_dim)
-    return forward_chunk(model, tokens, 0, kv, bf16_kv)
+    return forward_chunk(model, tokens, 0, kv, bf16_kv, want=first)
 
 
 def brute_force_prefix_logits(model, tokens, bf16_kv=False):
@@ -254,7 +257,7 @@ def teacher_forced_logits(model, prompt, outputs, bf16_kv=False):
     positions P-1 .. P+G-2 of prompt ++ outputs[:-1]."""
     seq = np.concatenate([np.asarray(prompt, dtype=np.int64),
                           np.asarray(outputs[:-1], dtype=np.int64)])
-    return forward_full(model, seq, bf16_kv)[len(prompt) - 1:]
+    return forward_full(model, seq, bf16_kv, first=len(prompt) - 1)
 
 
 def decode_from_history(model, K_hist, V_hist, token, pos, bf16_kv=False):

@@ -133,7 +133,7 @@ Layout make_layout(const moa_engine_cfg& c) {
   L.part_cap = pc;
   L.token_store = c.token_store ? c.token_store : (int64_t)64 << 20;
   L.block_store = c.block_store ? c.block_store : (int64_t)16 << 20;
-  L.meta_ints = 4 * L.Tmax + 2 * L.Rmax + 4 * L.items_cap + 4 * L.red_cap;
+  L.meta_ints = 4 * L.Tmax + 2 * L.Rmax + 8 * L.items_cap + 4 * L.red_cap + 4 * L.Tmax;
   L.block_bytes = (size_t)Lr * nkv * 2 * kBlock * hd * L.esz;
   L.kv_bytes = L.block_bytes * (size_t)c.num_kv_blocks;
   const size_t per_layer = (size_t)(2 * d + qkv * d + d * nh * hd + 3 * F * d) * L.esz;
@@ -224,6 +224,7 @@ struct moa_engine {
   std::vector<int> r_tok, r_pos, r_bt, r_model, l_src, l_dst;
   std::vector<AttnItem> items;
   std::vector<ReduceItem> red;
+  std::vector<PrefillItem> pitems;
 };
 
 namespace {
@@ -663,8 +664,8 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   if (st != MOA_OK) return st;
 
   // ---- stage: metadata, then prompts and block lists of admitted requests
-  const int nitems = (int)e->items.size(), nred = (int)e->red.size();
-  size_t meta_ints = 4 * (size_t)T + 2 * (size_t)R + 4 * (size_t)nitems + 4 * (size_t)nred;
+  const int nitems = (int)e->items.size(), nred = (int)e->red.size(), npre = (int)e->pitems.size();
+  size_t meta_ints = 4 * (size_t)T + 2 * (size_t)R + 8 * (size_t)nitems + 4 * (size_t)nred + 4 * (size_t)npre;
   size_t up_ints = 0;
   for (int64_t id : admitted) up_ints += e->reqs[id].prompt.size() + e->reqs[id].blocks.size();
   st = ensure_stage(e, slot, (meta_ints + up_ints) * 4);
@@ -678,8 +679,9 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   const size_t o_mod = o; put(e->r_model.data(), T);
   const size_t o_ls = o; put(e->l_src.data(), R);
   const size_t o_ld = o; put(e->l_dst.data(), R);
-  const size_t o_it = o; put(e->items.data(), 4 * (size_t)nitems);
+  const size_t o_it = o; put(e->items.data(), 8 * (size_t)nitems);
   const size_t o_rd = o; put(e->red.data(), 4 * (size_t)nred);
+  const size_t o_pi = o; put(e->pitems.data(), 4 * (size_t)npre);
   HIPCHK(hipMemcpyAsync(e->meta, hb, meta_ints * 4, hipMemcpyHostToDevice, e->stream), "meta upload");
   for (int64_t id : admitted) {
     Request& r = e->reqs[id];
@@ -702,6 +704,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   sd.lm_dst = e->meta + o_ld;
   sd.items = (const AttnItem*)(e->meta + o_it);
   sd.red = (const ReduceItem*)(e->meta + o_rd);
+  sd.pre = (const PrefillItem*)(e->meta + o_pi);
 
   // ---- kernels
   const bool bf = e->bf16;
@@ -751,6 +754,15 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
     kv_keys += it.k1 - it.k0;
     max_item_blocks = std::max(max_item_blocks, ((it.k1 - 1) >> 4) - (it.k0 >> 4) + 1);
   }
+  // causal prefill blocks: K/V of keys [0, pos0 + nq) once per KV head; q.k and p.v per (row, key <= pos)
+  double pre_keys = 0, pre_pairs = 0, pre_rows = 0;
+  for (const PrefillItem& pi : e->pitems) {
+    pre_keys += pi.pos0 + pi.nq;
+    pre_pairs += (double)pi.nq * pi.pos0 + (double)pi.nq * (pi.nq + 1) / 2;
+    pre_rows += pi.nq;
+  }
+  const double pre_bytes = pre_keys * nkv * 2.0 * hd * esz + pre_rows * nh * hd * 8.0;
+  const double pre_flops = pre_pairs * nh * hd * 4.0;
   const double attn_bytes = kv_keys * nkv * 2.0 * hd * esz + (double)T * nh * hd * 8.0;
   const double attn_flops = kv_keys * nh * hd * 4.0;
   const double norm_bytes = (double)T * d * 12.0;
@@ -776,10 +788,15 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
       LAUNCH(MOA_K_ROPE_KV, (double)T * qkv * 4.0 * ga.S + (double)T * (nh * hd * 4.0 + 2.0 * nkv * hd * esz), 0,
              launch_rope_kv(s, bf, e->part, ga.S, ga.out_split, sd.row_pos, sd.row_bt, e->bt_store, e->rope, e->q,
                             e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd, T), "rope kv");
-      LAUNCH(MOA_K_ATTN, attn_bytes, attn_flops,
-             launch_attention(s, bf, sd.items, nitems, max_item_blocks, e->q, e->kv, e->bt_store, sd.row_bt, l,
-                              e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc,
-                              e->pml), "attention");
+      if (npre > 0)
+        LAUNCH(MOA_K_PREFILL_ATTN, pre_bytes, pre_flops,
+               launch_prefill_attention(s, sd.pre, npre, e->q, e->kv, e->bt_store, l, e->cfg.num_kv_blocks, nh, nkv,
+                                        hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo), "prefill attention");
+      if (nitems > 0)
+        LAUNCH(MOA_K_ATTN, attn_bytes, attn_flops,
+               launch_attention(s, bf, sd.items, nitems, max_item_blocks, e->q, e->kv, e->bt_store, sd.row_bt, l,
+                                e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc,
+                                e->pml), "attention");
       if (nred > 0)
         LAUNCH(MOA_K_ATTN_REDUCE, (double)nslots_total(e) * nh * (hd + 2) * 4.0, 0,
                launch_attn_reduce(s, bf, sd.red, nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
@@ -900,7 +917,9 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
   // rows grouped by model: prefill chunks then decode rows, each in admission order
   const int T = n_pre + n_dec;
   e->r_tok.clear(); e->r_pos.clear(); e->r_bt.clear(); e->r_model.clear();
-  e->l_src.clear(); e->l_dst.clear(); e->items.clear(); e->red.clear();
+  e->l_src.clear(); e->l_dst.clear(); e->items.clear(); e->red.clear(); e->pitems.clear();
+  // bf16 engines run prompt chunks through the causal MFMA prefill kernel
+  const bool tiled_prefill = e->bf16 && (e->cfg.model.head_dim == 64 || e->cfg.model.head_dim == 128);
   int grp_rows[kMaxModels] = {0}, grp_lm[kMaxModels] = {0};
   int nslots = 0;
   std::vector<std::pair<int64_t, int>> capture_rows;   // (request, lm row)
@@ -919,16 +938,20 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
           e->r_model.push_back(m);
           grp_rows[m]++;
           const int ctx = pos + 1;
-          if (a.kind == 0) {
-            e->items.push_back({row, 0, ctx, -1});
+          const int bto = (int)r.bt_off;
+          if (a.kind == 0 && tiled_prefill) {
+            if (i % 64 == 0) e->pitems.push_back({row, pos, std::min(64, a.len - i), bto});
+          } else if (a.kind == 0) {
+            e->items.push_back({row, 0, ctx, -1, bto, 0, 0, 0});
           } else {
             const int ns = (ctx + kSplitKeys - 1) / kSplitKeys;
             if (ns == 1) {
-              e->items.push_back({row, 0, ctx, -1});
+              e->items.push_back({row, 0, ctx, -1, bto, 0, 0, 0});
             } else {
               e->red.push_back({row, nslots, ns, 0});
               for (int k = 0; k < ns; ++k)
-                e->items.push_back({row, k * kSplitKeys, std::min(ctx, (k + 1) * kSplitKeys), nslots + k});
+                e->items.push_back({row, k * kSplitKeys, std::min(ctx, (k + 1) * kSplitKeys), nslots + k,
+                                    bto + k * kSplitKeys / kBlock, 0, 0, 0});
               nslots += ns;
             }
           }

@@ -45,8 +45,14 @@ enum Epilogue { EPI_F32 = 0, EPI_SWIGLU = 1 };
 constexpr int kWgTile = 1000;
 
 // Attention work item: one query row against keys [k0, k1) of its request.
-struct AttnItem { int row, k0, k1, slot; };   // slot < 0: write the final output
+// bt_off: index in the block store of the block holding key k0 (k0 is a
+// multiple of 16). slot < 0: write the final output, else partial slot.
+struct AttnItem { int row, k0, k1, slot, bt_off, pad0, pad1, pad2; };
 struct ReduceItem { int row, slot0, nslots, pad; };
+// Causal prefill block: step rows [row0, row0 + nq) hold positions
+// [pos0, pos0 + nq) of one request (nq <= 64); keys [0, pos0 + nq).
+// bt_off: the request's block list in the block store.
+struct PrefillItem { int row0, pos0, nq, bt_off; };
 
 struct StepDev {
   const int* row_tok;    // [T] index into the token store
@@ -57,6 +63,7 @@ struct StepDev {
   const int* lm_dst;     // [R] token-store slot the token goes to
   const AttnItem* items; // attention items
   const ReduceItem* red; // split-combine items
+  const PrefillItem* pre;// causal prefill blocks
 };
 
 // Attach a start/stop event pair to the launches that follow (nullptr: none).
@@ -85,6 +92,11 @@ hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, in
                             const float* q, const void* kv, const int* bt_store, const int* row_bt,
                             int layer, int num_blocks, int n_h, int n_kv, int hd, float scale,
                             void* out, size_t out_lo, float* pacc, float* pml);
+
+// bf16 KV only, head_dim 64 or 128; writes split-bf16 rows of `out`.
+hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, int nitems, const float* q,
+                                   const void* kv, const int* bt_store, int layer, int num_blocks, int n_h,
+                                   int n_kv, int hd, float scale, void* out, size_t out_lo);
 
 hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, int nred,
                               const float* pacc, const float* pml, void* out, size_t out_lo, int n_h,

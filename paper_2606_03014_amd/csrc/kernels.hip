@@ -19,6 +19,7 @@ namespace moa {
 // timestamps the dispatch itself, so the measured span is the kernel's).
 static hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
 
+
 void set_launch_events(hipEvent_t start, hipEvent_t stop) {
   g_ev_start = start;
   g_ev_stop = stop;
@@ -60,6 +61,12 @@ __device__ __forceinline__ void store_split(uint16_t* p, size_t lo, size_t i, fl
   const uint16_t h = f2bf(v);
   p[i] = h;
   p[i + lo] = f2bf(v - bf2f(h));
+}
+
+// Order this wavefront's LDS writes before its later LDS reads (no workgroup barrier).
+__device__ __forceinline__ void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
 }
 
 __device__ __forceinline__ const void* pick(const ModelPtrs& mp, int m) {
@@ -561,7 +568,7 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
 
   const int b0 = it.k0 >> 4, nb = ((it.k1 - 1) >> 4) - b0 + 1;
   {
-    const int* bt = bt_store + row_bt[it.row] + b0;
+    const int* bt = bt_store + it.bt_off;
     for (int i = threadIdx.x; i < nb; i += NT) sbt[i] = bt[i];
   }
   float q[CH];
@@ -686,6 +693,197 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
         pml[((size_t)it.slot * n_h + h) * 2] = m;
         pml[((size_t)it.slot * n_h + h) * 2 + 1] = l;
       }
+    }
+  }
+}
+
+// ------------------------------------------ causal prefill attention (MFMA)
+// bf16 KV cache. A workgroup = one query head x a block of up to 64
+// consecutive prompt positions of one request (the rows of one prefill chunk
+// in this step); its 4 wavefronts own 16 query rows each. Keys run from 0 to
+// the block's last position in tiles of 64; per tile the workgroup stages K
+// (row-major, rows padded against bank conflicts) and V transposed (V^T:
+// head-dim rows, key columns) in LDS, and loads the next tile meanwhile.
+// Each wavefront then computes, on MFMA 16x16x32 with fp32 accumulation:
+//   S = Q K^T  (A = 16 query rows x 32 dims of q, pre-scaled by
+//               log2(e)/sqrt(hd), as split bf16 hi + lo; B = K fragments),
+// applies the causal mask and the online softmax on the fragments (an S or O
+// fragment holds rows 4*(l/16)+i of column l%16, so every row statistic
+// lives in the lanes that own that row), writes P to its own LDS slab, and
+//   O += P V   (A = P as split bf16 read back from the slab; B = V^T fragments).
+template <int HD>
+__global__ __launch_bounds__(256) void k_prefill_attn(const PrefillItem* __restrict__ items,
+                                                      const float* __restrict__ qv, const uint16_t* __restrict__ kv,
+                                                      const int* __restrict__ bt_store, int layer, int NB, int n_h,
+                                                      int n_kv, float scale_log2, uint16_t* __restrict__ out,
+                                                      size_t out_lo) {
+  constexpr int TK = 64;                    // keys per tile
+  constexpr int KS = HD / 32;               // MFMA k-steps over head_dim (S = Q K^T)
+  constexpr int NT = HD / 16;               // 16-dim output tiles (O = P V)
+  constexpr int KROW = HD * 2 + 16;         // padded bytes per K row in LDS
+  constexpr int VROW = TK * 2 + 16;         // padded bytes per V^T row in LDS
+  constexpr int CPK = HD / 8;               // 16-byte chunks per key row
+  constexpr int NCH = TK * CPK;             // chunks per tile (K or V)
+  constexpr int PER = NCH / 256;            // per thread (K and V each)
+  static_assert(PER >= 1 && PER * 256 == NCH, "tile");
+  __shared__ __align__(16) unsigned char sK[TK * KROW];
+  __shared__ __align__(16) unsigned char sVt[HD * VROW];
+  __shared__ __align__(16) float sP[4][16 * TK];
+
+  const PrefillItem it = items[blockIdx.x];
+  const int h = blockIdx.y;
+  const int gq = n_h / n_kv;
+  const int kvh = h / gq;
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int kmax = it.pos0 + it.nq;          // keys [0, kmax)
+  const size_t hs = (size_t)2 * kBlock * HD;
+  const uint16_t* pool = kv + ((size_t)layer * NB * n_kv + kvh) * hs;
+  const size_t bstride = (size_t)n_kv * hs;
+  const int* bt = bt_store + it.bt_off;
+
+  // q fragments for this wavefront's 16 rows (rows past nq read row nq-1: never stored)
+  u32x4 qh[KS], ql[KS];
+  {
+    const int r = min(16 * w + (lane & 15), it.nq - 1);
+    const float* qrow = qv + ((size_t)(it.row0 + r) * n_h + h) * HD;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      unsigned hv[4], lv[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x0 = qrow[ks * 32 + (lane >> 4) * 8 + 2 * j] * scale_log2;
+        const float x1 = qrow[ks * 32 + (lane >> 4) * 8 + 2 * j + 1] * scale_log2;
+        const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+        hv[j] = (unsigned)h0 | ((unsigned)h1 << 16);
+        lv[j] = (unsigned)f2bf(x0 - bf2f(h0)) | ((unsigned)f2bf(x1 - bf2f(h1)) << 16);
+      }
+      qh[ks] = u32x4{hv[0], hv[1], hv[2], hv[3]};
+      ql[ks] = u32x4{lv[0], lv[1], lv[2], lv[3]};
+    }
+  }
+  f32x4_t O[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float m[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { m[i] = -INFINITY; l[i] = 0.f; }
+  const int kl = lane & 15, rq = (lane >> 4) * 4;
+
+  u32x4 kc[PER], vc[PER];
+  auto fetch = [&](int t0) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = threadIdx.x + 256 * j;
+      const int key = c / CPK, cc = c - key * CPK;
+      const int p = t0 + key;
+      kc[j] = u32x4{0u, 0u, 0u, 0u};
+      vc[j] = u32x4{0u, 0u, 0u, 0u};
+      if (p < kmax) {
+        const uint16_t* base = pool + (size_t)bt[p >> 4] * bstride + (p & 15) * HD + cc * 8;
+        kc[j] = *(const u32x4*)base;
+        vc[j] = *(const u32x4*)(base + kBlock * HD);
+      }
+    }
+  };
+  fetch(0);
+  for (int t0 = 0; t0 < kmax; t0 += TK) {
+    __syncthreads();                                    // previous tile's LDS reads are done
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = threadIdx.x + 256 * j;
+      const int key = c / CPK, cc = c - key * CPK;
+      *(u32x4*)(sK + key * KROW + cc * 16) = kc[j];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {                     // V^T: element (dim, key)
+        const unsigned wv = vc[j][e];
+        *(uint16_t*)(sVt + (cc * 8 + 2 * e) * VROW + key * 2) = (uint16_t)(wv & 0xffffu);
+        *(uint16_t*)(sVt + (cc * 8 + 2 * e + 1) * VROW + key * 2) = (uint16_t)(wv >> 16);
+      }
+    }
+    __syncthreads();
+    if (t0 + TK < kmax) fetch(t0 + TK);
+    // S = Q K^T for the 4 key groups of the tile
+    f32x4_t S[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      S[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const u32x4 kb = *(const u32x4*)(sK + (16 * g + kl) * KROW + (ks * 32 + (lane >> 4) * 8) * 2);
+        S[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qh[ks]),
+                                                       __builtin_bit_cast(bf16x8_t, kb), S[g], 0, 0, 0);
+        S[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ql[ks]),
+                                                       __builtin_bit_cast(bf16x8_t, kb), S[g], 0, 0, 0);
+      }
+    }
+    // causal mask + online softmax; this lane owns rows rq+i (positions pos0 + 16w + rq + i)
+    float alpha[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int qpos = it.pos0 + 16 * w + rq + i;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int key = t0 + 16 * g + kl;
+        if (key > qpos || key >= kmax) S[g][i] = -INFINITY;
+        mx = fmaxf(mx, S[g][i]);
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      const float mn = fmaxf(m[i], mx);
+      // a row with no key yet (only possible for rows past nq) keeps m = -inf
+      const float base = (mn == -INFINITY) ? 0.f : mn;
+      alpha[i] = exp2f(m[i] - base);
+      float ts = 0.f;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float pj = exp2f(S[g][i] - base);
+        ts += pj;
+        sP[w][(rq + i) * TK + 16 * g + kl] = pj;
+      }
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) ts += __shfl_xor(ts, o, 64);
+      l[i] = l[i] * alpha[i] + ts;
+      m[i] = mn;
+    }
+#pragma unroll
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) O[n][i] *= alpha[i];
+    wave_lds_fence();
+    // O += P V over two 32-key k-steps
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const float* pr = &sP[w][kl * TK + ks * 32 + (lane >> 4) * 8];
+      unsigned ph[4], pl[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float x0 = pr[2 * j], x1 = pr[2 * j + 1];
+        const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+        ph[j] = (unsigned)h0 | ((unsigned)h1 << 16);
+        pl[j] = (unsigned)f2bf(x0 - bf2f(h0)) | ((unsigned)f2bf(x1 - bf2f(h1)) << 16);
+      }
+      const u32x4 pa = u32x4{ph[0], ph[1], ph[2], ph[3]}, pb = u32x4{pl[0], pl[1], pl[2], pl[3]};
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const u32x4 vb = *(const u32x4*)(sVt + (16 * n + kl) * VROW + (ks * 32 + (lane >> 4) * 8) * 2);
+        O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, pa),
+                                                       __builtin_bit_cast(bf16x8_t, vb), O[n], 0, 0, 0);
+        O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, pb),
+                                                       __builtin_bit_cast(bf16x8_t, vb), O[n], 0, 0, 0);
+      }
+    }
+    wave_lds_fence();
+  }
+  // normalise and store rows < nq (O fragment: row rq+i, dim 16n + kl)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 16 * w + rq + i;
+    if (r < it.nq) {
+      const float inv = 1.f / l[i];
+      const size_t o = ((size_t)(it.row0 + r) * n_h + h) * HD + kl;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) store_split(out, out_lo, o + 16 * n, O[n][i] * inv);
     }
   }
 }
@@ -861,6 +1059,7 @@ hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, in
                             int layer, int num_blocks, int n_h, int n_kv, int hd, float scale,
                             void* out, size_t out_lo, float* pacc, float* pml) {
   if (nitems <= 0) return hipSuccess;
+
   const unsigned shm = (unsigned)max_item_blocks * 4u;
   if (shm > 48u * 1024u) return hipErrorInvalidValue;
   const int gq = n_h / n_kv;
@@ -875,6 +1074,23 @@ hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, in
                 : attn_gq<128, false>(st, gq, grid, shm, items, q, kv, bt_store, row_bt, layer, num_blocks, n_h, n_kv, sl2, out, out_lo, pacc, pml);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, int nitems, const float* q,
+                                   const void* kv, const int* bt_store, int layer, int num_blocks, int n_h,
+                                   int n_kv, int hd, float scale, void* out, size_t out_lo) {
+  if (nitems <= 0) return hipSuccess;
+  const dim3 grid(nitems, n_h), blk(256);
+  const float sl2 = scale * 1.4426950408889634f;
+  if (hd == 64)
+    klaunch(k_prefill_attn<64>, grid, blk, st, items, q, (const uint16_t*)kv, bt_store, layer, num_blocks, n_h, n_kv,
+            sl2, (uint16_t*)out, out_lo);
+  else if (hd == 128)
+    klaunch(k_prefill_attn<128>, grid, blk, st, items, q, (const uint16_t*)kv, bt_store, layer, num_blocks, n_h,
+            n_kv, sl2, (uint16_t*)out, out_lo);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
 }
 
 hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, int nred,

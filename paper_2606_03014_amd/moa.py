@@ -55,7 +55,7 @@ class moa_kernel_stats(C.Structure):
 
 
 KERNEL_CLASSES = ["embed", "norm", "gemm_qkv", "rope_kv", "attn", "attn_reduce", "gemm_o",
-                  "gemm_gateup", "gemm_down", "gemm_lmhead", "argmax"]
+                  "gemm_gateup", "gemm_down", "gemm_lmhead", "argmax", "prefill_attn"]
 
 P = C.POINTER
 _SIGS = {

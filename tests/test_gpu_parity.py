@@ -152,3 +152,18 @@ def test_bf16_1b_full_depth_requests():
     for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
         err, flips = compare(c.model, w, p, t, lg, True, 2e-2, what=f"1b req{i}")
         say(f"1b full depth req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+
+
+def test_bf16_8b_width_long_prompt_chunked_prefill():
+    """Real 8B width, two layers, a 2,500-token prompt prefilled in chunks of
+    1,024 (causal prefill blocks across ~40 key tiles, chunk boundaries inside
+    blocks) next to a short request decoding past one 256-key split."""
+    shape = replace(LLAMA_8B, n_layers=2)
+    consts = EngineConsts(num_kv_blocks=512, max_num_seqs=8, max_prefill_tokens=1024, max_model_len=4096)
+    ws = [generate_weights(LLAMA_8B, "bf16", 1, 3, 0, n_layers=2)]
+    prompts = _prompts(shape.vocab, [2500, 200], 6)
+    reqs = [(prompts[0], 0, 3), (prompts[1], 0, 70)]
+    toks, logs = run_requests(shape, "bf16", consts, ws, reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, flips = compare(shape, ws[m], p, t, lg, True, 2e-2, what=f"long req{i}")
+        say(f"8b-wide long req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
