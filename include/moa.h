@@ -134,6 +134,22 @@ moa_status moa_load_expert(moa_engine* e, const moa_model_cfg* cfg, const void* 
 moa_status moa_submit(moa_engine* e, const int32_t* tokens, int32_t n_tokens, int32_t model_id,
                       int32_t max_new_tokens, int64_t* request_id);
 
+/* Queue a call that arrives with a KV history instead of a prompt to prefill
+ * (a long generation already in progress): positions 0..ctx_len-1 of every
+ * layer hold the given K/V, the call feeds seed_token at position ctx_len and
+ * emits exactly max_new_tokens tokens. It needs
+ * ceil((ctx_len + max_new_tokens) / 16) blocks and skips the prefill phase.
+ * host_kv: [n_layers][2 (K, V)][ctx_len][n_kv_heads][head_dim] elements of the
+ * engine dtype (K after RoPE), copied before the call returns and written into
+ * the request's blocks when it is admitted (that step drains the stream).
+ * host_kv == NULL: the history is filled on the device with values in
+ * [-1, 1) from a hash of (request id, layer, K|V, position, head, dim).
+ * EINVAL: bad id, ctx_len < 0, max_new_tokens < 1, seed token outside the
+ * vocabulary, or ctx_len + max_new_tokens > max_model_len. ENOSPC / ENOMEM as
+ * for moa_submit. */
+moa_status moa_submit_with_history(moa_engine* e, int32_t model_id, int32_t seed_token, int32_t ctx_len,
+                                   const void* host_kv, int32_t max_new_tokens, int64_t* request_id);
+
 /* Plan one step on the host and enqueue its kernels on the stream:
  *   1 admit FIFO heads while a seat and their blocks are free (head-of-line
  *     blocking); a request gets the smallest free block ids, ascending;

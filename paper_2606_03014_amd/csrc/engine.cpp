@@ -29,6 +29,12 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 struct Request {
   int64_t id = 0;
   int32_t model = 0, P = 0, G = 0, need = 0;
+  // Injected history: positions 0..shift-1 arrive as K/V, the seed token sits
+  // at position shift (P = shift + 1) and token-store slot tok_off holds it.
+  // Position p's token lives at slot tok_off + p - shift.
+  int32_t shift = 0;
+  bool history = false;
+  std::vector<char> host_kv;          // caller's K/V until admission (empty: device fill)
   int32_t pre = 0, gen = 0;
   bool fresh = false;
   int64_t tok_off = -1;               // token store: P prompt slots, then G outputs
@@ -629,7 +635,81 @@ moa_status moa_submit(moa_engine* e, const int32_t* tokens, int32_t n_tokens, in
   return MOA_OK;
 }
 
+moa_status moa_submit_with_history(moa_engine* e, int32_t model_id, int32_t seed_token, int32_t ctx_len,
+                                   const void* host_kv, int32_t max_new_tokens, int64_t* request_id) {
+  if (!e || !request_id) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (ctx_len < 0 || max_new_tokens < 1) return MOA_EINVAL;
+  if (model_id < 0 || model_id >= (int32_t)e->models.size()) return MOA_EINVAL;
+  if ((int64_t)ctx_len + max_new_tokens > e->cfg.max_model_len) return MOA_EINVAL;
+  if (!e->plan_only && (seed_token < 0 || seed_token >= e->cfg.model.vocab)) return MOA_EINVAL;
+  const int64_t need = ((int64_t)ctx_len + max_new_tokens + kBlock - 1) / kBlock;
+  if (need > e->cfg.num_kv_blocks) return MOA_ENOSPC;
+  if (e->live == 0) e->tok_top = 0, e->bt_top = 0;
+  if (e->tok_top + 1 + max_new_tokens > e->lay.token_store) return MOA_ENOMEM;
+  Request r;
+  r.id = (int64_t)e->reqs.size();
+  r.model = model_id;
+  r.shift = ctx_len;
+  r.P = ctx_len + 1;
+  r.pre = r.P;                        // nothing to prefill
+  r.G = max_new_tokens;
+  r.need = (int32_t)need;
+  r.history = true;
+  r.tok_off = e->tok_top;
+  e->tok_top += 1 + max_new_tokens;
+  r.prompt.assign(1, seed_token);
+  if (host_kv && ctx_len > 0 && !e->plan_only) {
+    const moa_model_cfg& g = e->cfg.model;
+    const size_t bytes = (size_t)g.n_layers * 2 * ctx_len * g.n_kv_heads * g.head_dim * e->lay.esz;
+    r.host_kv.assign((const char*)host_kv, (const char*)host_kv + bytes);
+  }
+  e->reqs.push_back(std::move(r));
+  e->pending.push_back(e->reqs.back().id);
+  e->live += 1;
+  *request_id = e->reqs.back().id;
+  return MOA_OK;
+}
+
 namespace {
+
+// Write the injected K/V history of admitted requests into their blocks.
+// With caller data: stage it through the logits buffer (idle between steps;
+// the stream is drained first) one (layer, K|V) position range at a time and
+// scatter it with a kernel. Without: fill on the device from a hash of
+// (request, layer, K|V, position, head, dim).
+moa_status write_histories(moa_engine* e, const std::vector<int64_t>& admitted) {
+  const moa_model_cfg& g = e->cfg.model;
+  const size_t esz = e->lay.esz;
+  const size_t row = (size_t)g.n_kv_heads * g.head_dim;             // elements per position
+  const size_t cap_rows = std::max<size_t>(1, (size_t)e->lay.Rmax * g.vocab * 4 / (row * esz));
+  bool drained = false;
+  for (int64_t id : admitted) {
+    Request& r = e->reqs[id];
+    if (!r.history || r.shift == 0) continue;
+    if (r.host_kv.empty()) {
+      HIPCHK(launch_kv_fill(e->stream, e->bf16, e->kv, e->bt_store + r.bt_off, r.shift, g.n_layers,
+                            e->cfg.num_kv_blocks, g.n_kv_heads, g.head_dim, (uint32_t)r.id), "history fill");
+      continue;
+    }
+    if (!drained) {
+      HIPCHK(hipStreamSynchronize(e->stream), "history sync");
+      drained = true;
+    }
+    for (int l = 0; l < g.n_layers; ++l)
+      for (int kv = 0; kv < 2; ++kv)
+        for (size_t p0 = 0; p0 < (size_t)r.shift; p0 += cap_rows) {
+          const size_t n = std::min(cap_rows, (size_t)r.shift - p0);
+          const char* src = r.host_kv.data() + (((size_t)l * 2 + kv) * r.shift + p0) * row * esz;
+          HIPCHK(hipMemcpy(e->logits, src, n * row * esz, hipMemcpyHostToDevice), "history upload");
+          HIPCHK(launch_kv_scatter(e->stream, e->bf16, e->logits, e->kv, e->bt_store + r.bt_off, (int)p0, (int)n, l,
+                                   kv, e->cfg.num_kv_blocks, g.n_kv_heads, g.head_dim), "history scatter");
+          HIPCHK(hipStreamSynchronize(e->stream), "history sync");
+        }
+    std::vector<char>().swap(r.host_kv);
+  }
+  return MOA_OK;
+}
 
 // Wait until staging slot `slot` is no longer read by an in-flight step.
 moa_status wait_slot(moa_engine* e, int slot) {
@@ -695,6 +775,8 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
            "block list upload");
     std::vector<int32_t>().swap(r.prompt);
   }
+  st = write_histories(e, admitted);
+  if (st != MOA_OK) return st;
   StepDev sd;
   sd.row_tok = e->meta + o_tok;
   sd.row_pos = e->meta + o_pos;
@@ -932,7 +1014,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
         for (int i = 0; i < a.len; ++i) {
           const int pos = a.start + i;
           const int row = (int)e->r_tok.size();
-          e->r_tok.push_back((int)(r.tok_off + pos));    // prompt slot, or output gen-1 for decode
+          e->r_tok.push_back((int)(r.tok_off + pos - r.shift));   // prompt slot, or output gen-1 for decode
           e->r_pos.push_back(pos);
           e->r_bt.push_back((int)r.bt_off);
           e->r_model.push_back(m);
@@ -959,7 +1041,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
           if (emits) {
             const int gen_idx = (a.kind == 1) ? (pos - r.P + 1) : 0;   // output index produced
             e->l_src.push_back(row);
-            e->l_dst.push_back((int)(r.tok_off + r.P + gen_idx));
+            e->l_dst.push_back((int)(r.tok_off + r.P - r.shift + gen_idx));
             grp_lm[m]++;
             if (r.capture) capture_rows.push_back({a.id, (int)e->l_src.size() - 1});
           }
@@ -980,7 +1062,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
     for (auto& cr : capture_rows) {
       Request& r = e->reqs[cr.first];
       const int row = cr.second;
-      const int gen_idx = e->l_dst[row] - (int)(r.tok_off + r.P);
+      const int gen_idx = e->l_dst[row] - (int)(r.tok_off + r.P - r.shift);
       hipError_t err = hipMemcpyAsync(r.capture + (size_t)gen_idx * e->cfg.model.vocab,
                                       e->logits + (size_t)row * e->cfg.model.vocab,
                                       (size_t)e->cfg.model.vocab * 4, hipMemcpyDeviceToHost, e->stream);
@@ -989,6 +1071,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
   } else {
     for (int64_t id : admitted) std::vector<int32_t>().swap(e->reqs[id].prompt);
   }
+  for (int64_t id : admitted) std::vector<char>().swap(e->reqs[id].host_kv);
   // 4 retire
   int n_ret = 0;
   std::vector<int64_t> keep;
@@ -1054,7 +1137,7 @@ moa_status moa_collect(moa_engine* e, int64_t upto_step, moa_result* res, int32_
     int64_t o = 0;
     for (int32_t i = 0; i < n; ++i) {
       const Request& r = e->reqs[e->done[i]];
-      HIPCHK(hipMemcpyAsync(e->pinned_out + o, e->tok_store + r.tok_off + r.P, (size_t)r.G * 4,
+      HIPCHK(hipMemcpyAsync(e->pinned_out + o, e->tok_store + r.tok_off + r.P - r.shift, (size_t)r.G * 4,
                             hipMemcpyDeviceToHost, e->copy_stream), "collect copy");
       o += r.G;
     }

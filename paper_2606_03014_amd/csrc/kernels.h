@@ -102,6 +102,15 @@ hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, 
                               const float* pacc, const float* pml, void* out, size_t out_lo, int n_h,
                               int hd);
 
+// Injected history. scatter: src [n][n_kv][hd] (engine dtype) -> positions
+// [p0, p0 + n) of plane (layer, kv: 0 K / 1 V) through the request's block list.
+// fill: positions [0, ctx) of every layer from a hash of (tag, layer, kv,
+// position, head, dim), values in [-1, 1).
+hipError_t launch_kv_scatter(hipStream_t st, bool bf16, const void* src, void* kv, const int* blocks, int p0, int n,
+                             int layer, int kv_sel, int num_blocks, int n_kv, int hd);
+hipError_t launch_kv_fill(hipStream_t st, bool bf16, void* kv, const int* blocks, int ctx, int n_layers,
+                          int num_blocks, int n_kv, int hd, uint32_t tag);
+
 hipError_t launch_argmax(hipStream_t st, const float* logits, int R, int V, const int* lm_dst,
                          int* tok_store);
 

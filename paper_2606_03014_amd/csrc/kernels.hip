@@ -950,7 +950,73 @@ __global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logit
   }
 }
 
+// ------------------------------------------------------ injected history
+template <typename T>
+__global__ __launch_bounds__(256) void k_kv_scatter(const T* __restrict__ src, T* __restrict__ kv,
+                                                    const int* __restrict__ blocks, int p0, int n, int layer,
+                                                    int kv_sel, int NB, int n_kv, int hd) {
+  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t per = (size_t)n_kv * hd;
+  if (e >= (size_t)n * per) return;
+  const int p = p0 + (int)(e / per);
+  const int rem = (int)(e % per);
+  const int h = rem / hd, d = rem - h * hd;
+  const size_t hs = (size_t)2 * kBlock * hd;
+  const size_t o = (((size_t)layer * NB + blocks[p >> 4]) * n_kv + h) * hs + (size_t)kv_sel * kBlock * hd +
+                   (p & 15) * hd + d;
+  kv[o] = src[e];
+}
+
+__device__ __forceinline__ uint32_t mix32(uint32_t x) {
+  x ^= x >> 16; x *= 0x7feb352du; x ^= x >> 15; x *= 0x846ca68bu; x ^= x >> 16;
+  return x;
+}
+
+template <bool BF>
+__global__ __launch_bounds__(256) void k_kv_fill(void* __restrict__ kvv, const int* __restrict__ blocks, int ctx,
+                                                 int NB, int n_kv, int hd, uint32_t tag) {
+  // grid.y = layer * 2 + (K|V)
+  const int layer = blockIdx.y >> 1, kv_sel = blockIdx.y & 1;
+  const size_t e = (size_t)blockIdx.x * 256 + threadIdx.x;
+  const size_t per = (size_t)n_kv * hd;
+  if (e >= (size_t)ctx * per) return;
+  const int p = (int)(e / per);
+  const int rem = (int)(e % per);
+  const int h = rem / hd, d = rem - h * hd;
+  const uint32_t u = mix32(tag * 0x9e3779b9u ^ mix32(((uint32_t)blockIdx.y << 24) ^ (uint32_t)p) ^ (uint32_t)(rem * 0x85ebca6bu));
+  const float v = (float)(int)(u >> 8) * (1.0f / 8388608.0f) - 1.0f;
+  const size_t hs = (size_t)2 * kBlock * hd;
+  const size_t o = (((size_t)layer * NB + blocks[p >> 4]) * n_kv + h) * hs + (size_t)kv_sel * kBlock * hd +
+                   (p & 15) * hd + d;
+  if (BF) ((uint16_t*)kvv)[o] = f2bf(v);
+  else ((float*)kvv)[o] = v;
+}
+
 // =============================================================== launchers
+
+hipError_t launch_kv_scatter(hipStream_t st, bool bf16, const void* src, void* kv, const int* blocks, int p0, int n,
+                             int layer, int kv_sel, int num_blocks, int n_kv, int hd) {
+  const size_t total = (size_t)n * n_kv * hd;
+  if (total == 0) return hipSuccess;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  if (bf16)
+    klaunch(k_kv_scatter<uint16_t>, grid, dim3(256), st, (const uint16_t*)src, (uint16_t*)kv, blocks, p0, n, layer,
+            kv_sel, num_blocks, n_kv, hd);
+  else
+    klaunch(k_kv_scatter<float>, grid, dim3(256), st, (const float*)src, (float*)kv, blocks, p0, n, layer, kv_sel,
+            num_blocks, n_kv, hd);
+  return hipGetLastError();
+}
+
+hipError_t launch_kv_fill(hipStream_t st, bool bf16, void* kv, const int* blocks, int ctx, int n_layers,
+                          int num_blocks, int n_kv, int hd, uint32_t tag) {
+  const size_t total = (size_t)ctx * n_kv * hd;
+  if (total == 0) return hipSuccess;
+  const dim3 grid((unsigned)((total + 255) / 256), 2 * n_layers);
+  if (bf16) klaunch(k_kv_fill<true>, grid, dim3(256), st, kv, blocks, ctx, num_blocks, n_kv, hd, tag);
+  else klaunch(k_kv_fill<false>, grid, dim3(256), st, kv, blocks, ctx, num_blocks, n_kv, hd, tag);
+  return hipGetLastError();
+}
 
 hipError_t launch_embed(hipStream_t st, bool bf16, const int* tok_store, const int* row_tok,
                         const int* row_model, ModelPtrs embed, float* x, int T, int d) {

@@ -53,6 +53,9 @@ class Engine:
     def submit(self, tokens, model_id, max_new):
         return M.moa_submit(self.h, tokens, model_id, max_new)
 
+    def submit_with_history(self, model_id, seed_token, ctx_len, max_new, host_kv=None):
+        return M.moa_submit_with_history(self.h, model_id, seed_token, ctx_len, max_new, host_kv)
+
     def step(self):
         return M.moa_step(self.h)
 
@@ -161,3 +164,39 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
         if max_steps is not None and res.n_steps >= max_steps:
             break
     return res
+
+
+def run_straggler(eng, sw, model_id=0, host_kv_fn=None, on_step=None):
+    """Drive the long-reasoning straggler workload: ``sw.n_live`` calls that
+    arrive with a KV history are submitted up front; for the first
+    ``sw.refill_steps`` steps every call that retires is replaced by a new one
+    (admitted at the next step), then the batch drains. host_kv_fn(i, L) may
+    return the K/V history of sequence i (None: device fill).
+    Returns (tokens generated, engine steps, sequences used)."""
+    nxt = 0
+
+    def submit_one():
+        nonlocal nxt
+        L, tok, R = sw.sequence(nxt)
+        kv = host_kv_fn(nxt, L) if host_kv_fn is not None else None
+        eng.submit_with_history(model_id, tok, L, R, kv)
+        nxt += 1
+        return R
+
+    tokens = 0
+    for _ in range(sw.n_live):
+        tokens += submit_one()
+    steps = 0
+    while True:
+        info = eng.step()
+        if info.step < 0:
+            break
+        steps += 1
+        if on_step is not None:
+            on_step(info)
+        if info.step < sw.refill_steps:
+            for _ in range(info.finished):
+                tokens += submit_one()
+        eng.collect(info.step - 1)
+    eng.collect(-1)
+    return tokens, steps, nxt

@@ -63,6 +63,8 @@ _SIGS = {
     "moa_create": (C.c_int, [P(moa_engine_cfg), C.c_void_p, C.c_size_t, C.c_void_p, P(C.c_void_p)]),
     "moa_load_expert": (C.c_int, [C.c_void_p, P(moa_model_cfg), C.c_void_p, C.c_size_t, P(C.c_int32)]),
     "moa_submit": (C.c_int, [C.c_void_p, P(C.c_int32), C.c_int32, C.c_int32, C.c_int32, P(C.c_int64)]),
+    "moa_submit_with_history": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int32,
+                                          P(C.c_int64)]),
     "moa_step": (C.c_int, [C.c_void_p, P(moa_step_info)]),
     "moa_collect": (C.c_int, [C.c_void_p, C.c_int64, P(moa_result), C.c_int32, P(C.c_int32),
                               P(C.c_int32), C.c_int64]),
@@ -140,6 +142,20 @@ def moa_submit(eng, tokens, model_id, max_new_tokens):
     rid = C.c_int64()
     check(lib().moa_submit(eng, t.ctypes.data_as(P(C.c_int32)), len(t), model_id, max_new_tokens,
                            C.byref(rid)), "moa_submit")
+    return rid.value
+
+
+def moa_submit_with_history(eng, model_id, seed_token, ctx_len, max_new_tokens, host_kv=None):
+    """host_kv: None (device fill) or a contiguous numpy array of
+    [n_layers, 2, ctx_len, n_kv_heads, head_dim] in the engine dtype."""
+    import numpy as np
+    rid = C.c_int64()
+    ptr = None
+    if host_kv is not None:
+        host_kv = np.ascontiguousarray(host_kv)
+        ptr = host_kv.ctypes.data_as(C.c_void_p)
+    check(lib().moa_submit_with_history(eng, model_id, seed_token, ctx_len, ptr, max_new_tokens, C.byref(rid)),
+          "moa_submit_with_history")
     return rid.value
 
 

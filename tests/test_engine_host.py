@@ -224,3 +224,56 @@ def test_random_small_workloads_bit_exact(seed):
     assert np.array_equal(eng.steps(), np.array(s.steps, dtype=np.int64).reshape(-1, 6))
     for req in s.reqs:
         assert eng.block_table(req.rid) == req.blocks
+
+
+def test_hand_traced_injected_history_matches():
+    ex = GOLD["examples"][1]
+    consts = EngineConsts(ex["num_blocks"], ex["max_num_seqs"], 16, 1000)
+    eng = _dry(TOY, consts, ex["n_models"])
+    for kind, m, L, R in ex["submit"]:
+        assert kind == "inj"
+        eng.submit_with_history(m, 1, L, R)
+    while eng.step().step >= 0:
+        pass
+    st = eng.steps()
+    assert len(st) == ex["n_steps"]
+    assert st[: len(ex["steps_head"])].tolist() == ex["steps_head"]
+    for rid, want in enumerate(ex["requests"]):
+        info = eng.request(rid)
+        assert (info.admit_step, info.finish_step) == (want["admit"], want["finish"])
+        assert eng.block_table(rid) == want["blocks"]
+        assert eng.chunks(rid) == []
+
+
+def test_straggler_workload_bookkeeping_is_bit_exact():
+    """Refill phase (every retired call replaced at the next admission) then
+    drain, against the oracle scheduler driven the same way."""
+    from moa_inputs import make_straggler_workload
+    from paper_2606_03014_amd.engine import run_straggler
+    c = CONFIGS["straggler-8b-bf16"]
+    sw = make_straggler_workload(0, n_live=512, refill_steps=64)
+    eng = _dry(c.model, c.engine, 1, "bf16")
+    tokens, steps, used = run_straggler(eng, sw)
+    s = OracleScheduler(c.engine.num_kv_blocks, c.engine.max_num_seqs, c.engine.max_prefill_tokens, 1,
+                        max_model_len=c.engine.max_model_len)
+    nxt = 0
+    for _ in range(sw.n_live):
+        L, tok, R = sw.sequence(nxt)
+        s.submit_injected(0, L, R)
+        nxt += 1
+    while True:
+        st = s.step()
+        if st is None:
+            break
+        if st < sw.refill_steps:
+            for _ in range(s.steps[-1][4]):
+                L, tok, R = sw.sequence(nxt)
+                s.submit_injected(0, L, R)
+                nxt += 1
+    assert used == nxt and steps == len(s.steps)
+    assert np.array_equal(eng.steps(), np.array(s.steps, dtype=np.int64))
+    for req in s.reqs[::17]:
+        info = eng.request(req.rid)
+        assert (info.admit_step, info.finish_step) == (req.admit_step, req.finish_step)
+        assert eng.block_table(req.rid) == req.blocks
+    assert tokens == sum(r.G for r in s.reqs)

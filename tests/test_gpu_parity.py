@@ -167,3 +167,54 @@ def test_bf16_8b_width_long_prompt_chunked_prefill():
     for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
         err, flips = compare(shape, ws[m], p, t, lg, True, 2e-2, what=f"long req{i}")
         say(f"8b-wide long req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+
+
+def test_bf16_injected_history_pareto_lengths():
+    """Calls that arrive with a bf16 K/V history (straggler workload): real
+    8B width, two layers, histories at quantiles of the Pareto(1.2) length law
+    up to the 32,768 cap; a few decode steps each, teacher-forced against the
+    oracle whose cache starts from the same history."""
+    from moa_inputs import f32_to_bf16_bits
+    from moa_inputs.workload import synthetic_kv
+    shape = replace(LLAMA_8B, n_layers=2)
+    consts = EngineConsts(num_kv_blocks=4096, max_num_seqs=16, max_prefill_tokens=64, max_model_len=32800)
+    w = generate_weights(LLAMA_8B, "bf16", 2, 4, 0, n_layers=2)
+    Ls = [0, 1, 255, 256, 300, 1051, 4000, 16383, 32768]
+    rng = np.random.default_rng(9)
+    seeds = [int(x) for x in rng.integers(0, shape.vocab, len(Ls))]
+    Rs = [3, 2, 4, 3, 2, 3, 2, 2, 3]
+    hist = []
+    eng = Engine(shape, "bf16", consts, 1)
+    try:
+        mid = eng.load(pack_blob(w, shape))
+        rids, caps = [], []
+        for i, (L, tok, R) in enumerate(zip(Ls, seeds, Rs)):
+            kv = synthetic_kv(0, i, 2, L, shape.n_kv_heads, shape.head_dim)
+            kvb = f32_to_bf16_bits(kv)
+            hist.append(kvb)
+            rid = eng.submit_with_history(mid, tok, L, R, kvb if L else None)
+            cap = np.full(R * shape.vocab, np.nan, dtype=np.float32)
+            eng.capture_logits(rid, cap)
+            rids.append(rid)
+            caps.append(cap)
+        say("injected histories submitted")
+        while eng.step().step >= 0:
+            pass
+        got = {r[0]: r[3] for r in eng.collect()}
+    finally:
+        eng.close()
+    om = T.OracleModel(shape, w, cache=False)
+    for i, (L, tok, R) in enumerate(zip(Ls, seeds, Rs)):
+        toks = got[rids[i]]
+        assert len(toks) == R
+        kv = T.ContiguousKV(2, shape.n_kv_heads, shape.head_dim)
+        for layer in range(2):
+            kv.K[layer] = T.to_f64(hist[i][layer, 0])
+            kv.V[layer] = T.to_f64(hist[i][layer, 1])
+        seq = [tok] + [int(t) for t in toks[:-1]]
+        ref = T.forward_chunk(om, seq, L, kv, bf16_kv=True)
+        lg = caps[i].reshape(R, -1)
+        err = float(np.abs(lg - ref).max())
+        flips = check_tokens(ref, toks, f"history L={L}")
+        say(f"history L={L} R={R}: |engine - oracle| {err:.3e} flips {flips}")
+        assert err <= 2e-2
