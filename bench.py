@@ -34,6 +34,23 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def measured_traffic(kernel):
+    """HBM bytes per launch of ``kernel`` from the committed rocprofv3 counter
+    summary, or None when none exists or the kernel source changed since."""
+    import glob
+    import hashlib
+    src = os.path.join(ROOT, "paper_2606_03014_amd", "csrc", "kernels.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*traffic*.md")):
+        for line in open(path):
+            line = line.strip()
+            if line.startswith("{") and '"traffic_bytes_per_launch"' in line:
+                rec = json.loads(line)
+                if rec.get("kernel") == kernel and rec.get("kernels_source_sha256_16") == sha:
+                    return rec["traffic_bytes_per_launch"]
+    return None
+
+
 def cpu_baseline(cfg, wl, weights0, budget_s):
     """The oracle, as it stands, on the first expert-0 call of the workload:
     prefill its prompt, then decode until the time budget runs out."""
@@ -74,7 +91,19 @@ def main():
     ap.add_argument("--time-every", type=int, default=8, help="time the kernels of 1 step in N")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized device buffer 8 times (HBM counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_probe:
+        import torch
+        n = args.copy_probe << 20
+        a = torch.empty(n, dtype=torch.uint8, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(8):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 8}))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
               "multi-GPU path: the engine runs every model of the batch on one MI355X.", file=sys.stderr)
@@ -147,7 +176,7 @@ def main():
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dom_name)
     roof["kernel"] = dom_name
     roof["launches_timed"] = dom["launches"]
     roof["us_per_launch"] = dom["ms"] / max(dom["launches"], 1) * 1e3
