@@ -77,6 +77,35 @@ __device__ __forceinline__ const void* pick(const ModelPtrs& mp, int m) {
   return r;
 }
 
+// Cross-lane moves inside a row of 16 lanes as DPP operand modifiers (plain
+// VALU, no LDS crossbar): quad_perm [1,0,3,2] = lane ^ 1, quad_perm [2,3,0,1]
+// = lane ^ 2, row_half_mirror = lane 7 - i within each 8 lanes (after the
+// two quad steps every lane of a quad holds the quad's value, so the mirror
+// brings in the other quad), row_ror:8 = lane ^ 8 within 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float sum8(float v) {       // over lanes 8k..8k+7
+  v += dpp<0xB1>(v);
+  v += dpp<0x4E>(v);
+  return v + dpp<0x141>(v);
+}
+__device__ __forceinline__ float sum16(float v) {      // over lanes 16k..16k+15
+  v = sum8(v);
+  return v + dpp<0x128>(v);
+}
+__device__ __forceinline__ float max16(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  return fmaxf(v, dpp<0x128>(v));
+}
+// lane ^ 16 (within 32 lanes) through ds_swizzle's bit mode
+__device__ __forceinline__ float swz_xor16(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
@@ -633,16 +662,14 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
 #pragma unroll
         for (int i = 0; i < CH; ++i) dot = fmaf(q[i], kr[i], dot);
       }
-      dot += __shfl_xor(dot, 1, 64);
-      dot += __shfl_xor(dot, 2, 64);
-      dot += __shfl_xor(dot, 4, 64);
+      dot = sum8(dot);
       s[p8] = (t0 + key < it.k1) ? dot * scale_log2 : -INFINITY;
     }
     float mx = s[0];
 #pragma unroll
     for (int p8 = 1; p8 < 8; ++p8) mx = fmaxf(mx, s[p8]);
-    mx = fmaxf(mx, __shfl_xor(mx, 8, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, dpp<0x128>(mx));
+    mx = fmaxf(mx, swz_xor16(mx));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mnew = fmaxf(m, mx);
     const float alpha = exp2f(m - mnew);
@@ -828,8 +855,7 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const PrefillItem* __restr
         if (key > qpos || key >= kmax) S[g][i] = -INFINITY;
         mx = fmaxf(mx, S[g][i]);
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      mx = max16(mx);
       const float mn = fmaxf(m[i], mx);
       // a row with no key yet (only possible for rows past nq) keeps m = -inf
       const float base = (mn == -INFINITY) ? 0.f : mn;
@@ -841,8 +867,7 @@ __global__ __launch_bounds__(256) void k_prefill_attn(const PrefillItem* __restr
         ts += pj;
         sP[w][(rq + i) * TK + 16 * g + kl] = pj;
       }
-#pragma unroll
-      for (int o = 1; o < 16; o <<= 1) ts += __shfl_xor(ts, o, 64);
+      ts = sum16(ts);
       l[i] = l[i] * alpha[i] + ts;
       m[i] = mn;
     }
