@@ -51,33 +51,266 @@ def measured_traffic(kernel):
     return None
 
 
-def cpu_baseline(cfg, wl, weights0, budget_s):
-    """The oracle, as it stands, on the first expert-0 call of the workload:
-    prefill its prompt, then decode until the time budget runs out."""
-    import numpy as np
-    from oracle import transformer as T
+def oracle_threads():
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
     except Exception:
-        threads = os.cpu_count()
+        return os.cpu_count()
+
+
+def cpu_baseline(cfg, wl, weights0, budget_s):
+    """The oracle, as it stands, on the workload's first call of model 0 (an
+    expert call, or the first aggregator call when there are no experts):
+    prefill its prompt in chunks of 256 positions (stopping after half the
+    budget if the prompt is that long), then decode until the budget runs out."""
+    from oracle import transformer as T
     om = T.OracleModel(cfg.model, weights0)
     for name in weights0:                       # fp64 upcast of the weights: setup, not timed
         om.W(name)
-    q, e, G = next(r for r in wl.expert_requests() if r[1] == 0)
+    reqs = [r for r in wl.expert_requests() if r[1] == 0]
+    q, G = (reqs[0][0], reqs[0][2]) if reqs else (0, wl.agg_max_new)
     prompt = wl.prompts[q]
     kv = T.ContiguousKV(cfg.model.n_layers, cfg.model.n_kv_heads, cfg.model.head_dim)
     t0 = time.perf_counter()
-    lg = T.forward_chunk(om, prompt, 0, kv, bf16_kv=True, want="last")[-1]
+    pos = 0
+    while pos < len(prompt):
+        c = min(256, len(prompt) - pos)
+        lg = T.forward_chunk(om, prompt[pos:pos + c], pos, kv, bf16_kv=True, want="last")[-1]
+        pos += c
+        if time.perf_counter() - t0 > budget_s / 2:
+            break
+    t_pre = time.perf_counter() - t0
     toks = [T.argmax_lowest(lg)]
     while len(toks) < G and time.perf_counter() - t0 < budget_s:
-        lg = T.forward_chunk(om, [toks[-1]], len(prompt) + len(toks) - 1, kv, bf16_kv=True)[-1]
+        lg = T.forward_chunk(om, [toks[-1]], pos + len(toks) - 1, kv, bf16_kv=True)[-1]
         toks.append(T.argmax_lowest(lg))
     dt = time.perf_counter() - t0
-    return {"value": len(toks) / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"expert 0 call of query {q}: prefill of {len(prompt)} prompt tokens plus "
-                       f"{len(toks) - 1} decode steps ({len(toks)} generated tokens, {dt:.1f} s, "
-                       f"fp64 numpy oracle with a KV cache)")}
+    return {"value": len(toks) / dt, "unit": "tokens/s", "cores": oracle_threads(), "kind": "oracle",
+            "sample": (f"model-0 call of query {q}: prefill of {pos} of its {len(prompt)} prompt tokens "
+                       f"({t_pre:.1f} s) plus {len(toks) - 1} decode steps ({len(toks)} generated tokens, "
+                       f"{dt:.1f} s, fp64 numpy oracle with a KV cache)")}
+
+
+def cpu_baseline_history(cfg, seed, weights0, budget_s):
+    """The oracle on the straggler workload's first sequence: its synthetic
+    K/V history (bf16-rounded) in a contiguous cache, then decode steps until
+    the budget or its remaining length runs out."""
+    import numpy as np
+    from moa_inputs import make_straggler_workload, synthetic_kv, f32_to_bf16_bits
+    from moa_inputs.weights import bf16_bits_to_f32
+    from oracle import transformer as T
+    m = cfg.model
+    om = T.OracleModel(m, weights0)
+    for name in weights0:
+        om.W(name)
+    L, tok, R = make_straggler_workload(seed).sequence(0)
+    hist = bf16_bits_to_f32(f32_to_bf16_bits(synthetic_kv(seed, 0, m.n_layers, L, m.n_kv_heads, m.head_dim)))
+    kv = T.ContiguousKV(m.n_layers, m.n_kv_heads, m.head_dim)
+    for l in range(m.n_layers):
+        kv.K[l] = hist[l, 0].astype(np.float64)
+        kv.V[l] = hist[l, 1].astype(np.float64)
+    del hist
+    t0 = time.perf_counter()
+    toks = [tok]
+    while len(toks) <= R and time.perf_counter() - t0 < budget_s:
+        lg = T.forward_chunk(om, [toks[-1]], L + len(toks) - 1, kv, bf16_kv=True)[-1]
+        toks.append(T.argmax_lowest(lg))
+    dt = time.perf_counter() - t0
+    n = len(toks) - 1
+    return {"value": n / dt, "unit": "tokens/s", "cores": oracle_threads(), "kind": "oracle",
+            "sample": (f"sequence 0 (KV history {L} positions, synthetic): {n} decode steps in {dt:.1f} s, "
+                       f"fp64 numpy oracle with a KV cache")}
+
+
+def kernel_summary(stats, label=""):
+    """Log per-class shares and rates; return the roofline object of the
+    class with the largest timed share (None when nothing was timed)."""
+    total_timed = sum(s["ms"] for s in stats.values())
+    if total_timed <= 0:
+        return None
+    for name, s in sorted(stats.items(), key=lambda kv: -kv[1]["ms"]):
+        if s["launches"]:
+            log(f"[bench] {label}{name:12s} {100 * s['ms'] / total_timed:5.1f}% of timed  "
+                f"{s['ms'] / s['launches'] * 1e3:8.1f} us/launch  "
+                f"{s['bytes'] / (s['ms'] * 1e-3) / 1e9:8.1f} GB/s  {s['flops'] / (s['ms'] * 1e-3) / 1e12:7.1f} TF/s")
+    dom_name, dom = max(stats.items(), key=lambda kv: kv[1]["ms"])
+    intensity = dom["flops"] / max(dom["bytes"], 1.0)
+    if intensity > MFMA_BF16_PEAK / HBM_PEAK:
+        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s"}
+    else:
+        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = measured_traffic(dom_name)
+    roof["kernel"] = dom_name
+    roof["launches_timed"] = dom["launches"]
+    roof["us_per_launch"] = dom["ms"] / max(dom["launches"], 1) * 1e3
+    roof["algorithmic_bytes_per_launch"] = dom["bytes"] / max(dom["launches"], 1)
+    roof["algorithmic_flops_per_launch"] = dom["flops"] / max(dom["launches"], 1)
+    return roof
+
+
+def class_rates(stats):
+    """Per-class achieved rates against the HBM and MFMA peaks."""
+    out = {}
+    for name, s in stats.items():
+        if s["launches"] and s["ms"] > 0:
+            sec = s["ms"] * 1e-3
+            out[name] = {"us_per_launch": round(s["ms"] / s["launches"] * 1e3, 2),
+                         "hbm_frac": round(s["bytes"] / sec / HBM_PEAK, 4),
+                         "mfma_frac": round(s["flops"] / sec / MFMA_BF16_PEAK, 4)}
+    return out
+
+
+class Progress:
+    """Logs an engine-step progress line at most every ``every_s`` seconds."""
+
+    def __init__(self, every_s=10.0):
+        self.every_s = every_s
+        self.reset()
+
+    def reset(self):
+        self.t0 = self.last = time.perf_counter()
+
+    def __call__(self, info):
+        now = time.perf_counter()
+        if now - self.last >= self.every_s:
+            self.last = now
+            log(f"[bench]   engine step {info.step}: running {info.running}, pending {info.pending}, "
+                f"{now - self.t0:.1f} s")
+
+
+def load_models(eng, cfg, seed, n_models):
+    """Generate and load each model's weights in turn (host copies freed as
+    they go: an 8B-shape blob is 16 GB)."""
+    from moa_inputs import generate_weights, pack_blob
+    mids, first = [], None
+    for m in range(n_models):
+        t = time.perf_counter()
+        w = generate_weights(cfg.model, cfg.dtype, seed, cfg.wid, m, threads=16)
+        blob = pack_blob(w, cfg.model)
+        mids.append(eng.load(blob))
+        if m == 0:
+            first = w
+        del w, blob
+        log(f"[bench] model {m} generated and loaded in {time.perf_counter() - t:.1f} s")
+    return mids, first
+
+
+def bench_feeder(args, cfg, eng, mids):
+    """Every routed expert call (and aggregator call) of the workload, run to
+    completion through the feeder; returns (tokens, seconds, extra)."""
+    import torch
+    from moa_inputs import make_workload
+    from paper_2606_03014_amd import run_feeder
+    wl = make_workload(cfg.name, args.seed, n_queries=args.queries)
+    log(f"[bench] {cfg.name}: {wl.n_queries} queries, {len(wl.max_new)} expert calls, "
+        f"{sum(len(p) for p in wl.prompts)} query prompt tokens")
+    agg = mids[cfg.n_experts] if cfg.aggregator else -1
+    prog = Progress()
+    phase = {"prefill_steps": 0, "prefill_tokens": 0, "decode_rows": 0, "steps": 0}
+
+    def on_step(info):
+        prog(info)
+        phase["steps"] += 1
+        phase["prefill_tokens"] += info.prefill_tokens
+        phase["decode_rows"] += info.decode_rows
+        phase["prefill_steps"] += 1 if info.prefill_tokens else 0
+
+    def one_step():
+        prog.reset()
+        for k in phase:
+            phase[k] = 0
+        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step)
+
+    for i in range(args.warmup):
+        t = time.perf_counter()
+        r = one_step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i}: {r.n_steps} engine steps, {r.tokens} tokens, {time.perf_counter() - t:.2f} s")
+    eng.time_kernels(args.time_every, HBM_PEAK, MFMA_BF16_PEAK)
+    torch.cuda.synchronize()
+    tokens = steps = prefill_tokens = 0
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        r = one_step()
+        tokens += r.tokens
+        steps += r.n_steps
+        prefill_tokens += phase["prefill_tokens"]
+        log(f"[bench] step {i}: {r.n_steps} engine steps ({phase['prefill_steps']} with prefill), "
+            f"{r.tokens} tokens, {phase['prefill_tokens']} prompt tokens prefilled")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    config = {"workload": cfg.name, "models": len(mids), "queries": wl.n_queries,
+              "expert_calls": len(wl.max_new), "generated_tokens_per_step": tokens // args.steps,
+              "prefill_tokens_per_step": prefill_tokens // args.steps,
+              "engine_steps_per_step": steps // args.steps, "seed": args.seed,
+              "parallelism": "single GPU"}
+    extra = {"prefill_tokens_per_s": prefill_tokens / wall}
+    return tokens, wall, config, extra, wl
+
+
+def bench_straggler(args, cfg, eng, mids):
+    """Long-reasoning straggler stress: a refill phase (every retired call is
+    replaced at the next step) then a drain phase; both reported."""
+    import torch
+    from moa_inputs import make_straggler_workload
+    from paper_2606_03014_amd import run_straggler
+    sw = make_straggler_workload(args.seed, n_live=args.queries)
+    prog = Progress()
+    marks = {}
+
+    def on_step(info):
+        prog(info)
+        rows = marks.setdefault("rows", [])
+        rows.append(info.decode_rows)
+        base = marks.setdefault("base", info.step)
+        if info.step - base == sw.refill_steps:          # every refill-phase step has finished
+            marks["t_refill_end"] = time.perf_counter()
+            marks["tokens_refill"] = sum(rows[:-1])
+
+    def one_step():
+        prog.reset()
+        marks.clear()
+        return run_straggler(eng, sw, mids[0], on_step=on_step, after_collect=True)
+
+    for i in range(args.warmup):
+        t = time.perf_counter()
+        tok, n, used = one_step()
+        torch.cuda.synchronize()
+        log(f"[bench] warmup {i}: {n} engine steps, {tok} tokens, {used} sequences, {time.perf_counter() - t:.2f} s")
+    eng.time_kernels(args.time_every, HBM_PEAK, MFMA_BF16_PEAK)
+    torch.cuda.synchronize()
+    tokens = steps = 0
+    phases = []
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        ts = time.perf_counter()
+        tok, n, used = one_step()
+        torch.cuda.synchronize()
+        te = time.perf_counter()
+        tokens += tok
+        steps += n
+        rows = marks["rows"]
+        ta = marks["t_refill_end"] - ts
+        ka = marks["tokens_refill"]
+        phases.append({"refill": {"steps": sw.refill_steps, "tokens": ka, "s": ta, "tokens_per_s": ka / ta,
+                                  "mean_live": ka / sw.refill_steps},
+                       "drain": {"steps": n - sw.refill_steps, "tokens": tok - ka, "s": te - ts - ta,
+                                 "tokens_per_s": (tok - ka) / (te - ts - ta),
+                                 "mean_live": (tok - ka) / max(n - sw.refill_steps, 1)}})
+        log(f"[bench] step {i}: {n} engine steps, {tok} tokens, {used} sequences; refill phase "
+            f"{ka} tokens in {ta:.2f} s, drain {tok - ka} tokens in {te - ts - ta:.2f} s; rows "
+            f"max {max(rows)} mean {sum(rows) / len(rows):.0f}")
+    wall = time.perf_counter() - t0
+    config = {"workload": cfg.name, "models": 1, "live_sequences": sw.n_live,
+              "refill_steps": sw.refill_steps, "generated_tokens_per_step": tokens // args.steps,
+              "engine_steps_per_step": steps // args.steps, "seed": args.seed,
+              "kv_history": "device-filled synthetic K/V (hash of seed, layer, position)",
+              "parallelism": "single GPU"}
+    return tokens, wall, config, {"phases": phases}, None
 
 
 def main():
@@ -109,78 +342,20 @@ def main():
               "multi-GPU path: the engine runs every model of the batch on one MI355X.", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
-    from moa_inputs import CONFIGS, generate_weights, make_workload, pack_blob
-    from paper_2606_03014_amd import Engine, run_feeder
+    from moa_inputs import CONFIGS
+    from paper_2606_03014_amd import Engine
 
     cfg = CONFIGS[args.workload]
-    wl = make_workload(cfg.name, args.seed, n_queries=args.queries)
+    straggler = cfg.name.startswith("straggler")
     n_models = cfg.n_experts + (1 if cfg.aggregator else 0)
-    log(f"[bench] {cfg.name}: {wl.n_queries} queries, {len(wl.max_new)} expert calls, {n_models} models")
-    t = time.perf_counter()
-    weights = [generate_weights(cfg.model, cfg.dtype, args.seed, cfg.wid, m) for m in range(n_models)]
-    log(f"[bench] weights generated in {time.perf_counter() - t:.1f} s")
     eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models)
-    t = time.perf_counter()
-    mids = [eng.load(pack_blob(w, cfg.model)) for w in weights]
-    log(f"[bench] weights loaded in {time.perf_counter() - t:.1f} s; arena {eng.arena_bytes / 2**30:.1f} GiB")
-    agg = mids[cfg.n_experts] if cfg.aggregator else -1
-
-    t_start = [time.perf_counter()]
-
-    def progress(info):
-        if info.step % 1000 == 0:
-            log(f"[bench]   engine step {info.step}: running {info.running}, pending {info.pending}, "
-                f"{time.perf_counter() - t_start[0]:.1f} s")
-
-    def one_step():
-        t_start[0] = time.perf_counter()
-        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=progress)
-
-    for i in range(args.warmup):
-        t = time.perf_counter()
-        r = one_step()
-        torch.cuda.synchronize()
-        log(f"[bench] warmup {i}: {r.n_steps} engine steps, {r.tokens} tokens, {time.perf_counter() - t:.2f} s")
-
-    eng.time_kernels(args.time_every, HBM_PEAK, MFMA_BF16_PEAK)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    tokens = 0
-    n_engine_steps = 0
-    for i in range(args.steps):
-        r = one_step()
-        tokens += r.tokens
-        n_engine_steps += r.n_steps
-        log(f"[bench] step {i}: {r.n_steps} engine steps, {r.tokens} tokens")
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    wall = t1 - t0
+    log(f"[bench] {cfg.name}: {n_models} model(s); arena {eng.arena_bytes / 2**30:.1f} GiB")
+    mids, weights0 = load_models(eng, cfg, args.seed, n_models)
+    run = bench_straggler if straggler else bench_feeder
+    tokens, wall, config, extra, wl = run(args, cfg, eng, mids)
     stats = eng.kernel_stats()
-
-    # kernel classes by timed share; per-class achieved rates
-    total_timed = sum(s["ms"] for s in stats.values()) or 1.0
-    for name, s in sorted(stats.items(), key=lambda kv: -kv[1]["ms"]):
-        if s["launches"]:
-            log(f"[bench] {name:12s} {100 * s['ms'] / total_timed:5.1f}% of timed  "
-                f"{s['ms'] / s['launches'] * 1e3:8.1f} us/launch  "
-                f"{s['bytes'] / (s['ms'] * 1e-3) / 1e9:8.1f} GB/s  {s['flops'] / (s['ms'] * 1e-3) / 1e12:7.1f} TF/s")
-    dom_name, dom = max(stats.items(), key=lambda kv: kv[1]["ms"])
-    intensity = dom["flops"] / max(dom["bytes"], 1.0)
-    mfma_bound = intensity > MFMA_BF16_PEAK / HBM_PEAK
-    if mfma_bound:
-        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s"}
-    else:
-        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(dom_name)
-    roof["kernel"] = dom_name
-    roof["launches_timed"] = dom["launches"]
-    roof["us_per_launch"] = dom["ms"] / max(dom["launches"], 1) * 1e3
-    roof["algorithmic_bytes_per_launch"] = dom["bytes"] / max(dom["launches"], 1)
+    roof = kernel_summary(stats)
     run_roof_ms = sum(s["roof_ms_all"] for s in stats.values())
 
     out = {
@@ -196,19 +371,21 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic",
-        "config": {"workload": cfg.name, "models": n_models, "queries": wl.n_queries,
-                   "expert_calls": len(wl.max_new), "generated_tokens_per_step": tokens // args.steps,
-                   "engine_steps_per_step": n_engine_steps // args.steps, "seed": args.seed,
-                   "parallelism": "single GPU"},
+        "config": config,
         "roofline": roof,
         "run_roofline": {"roof_ms": run_roof_ms / args.steps, "measured_ms": wall * 1e3 / args.steps,
                          "frac": run_roof_ms / (wall * 1e3)},
+        "kernel_classes": class_rates(stats),
     }
+    out.update(extra)
     eng.close()
     del eng
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, wl, weights[0], args.cpu_budget)
+        if straggler:
+            out["cpu_baseline"] = cpu_baseline_history(cfg, args.seed, weights0, args.cpu_budget)
+        else:
+            out["cpu_baseline"] = cpu_baseline(cfg, wl, weights0, args.cpu_budget)
     print(json.dumps(out), flush=True)
 
 

@@ -166,12 +166,14 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
     return res
 
 
-def run_straggler(eng, sw, model_id=0, host_kv_fn=None, on_step=None):
+def run_straggler(eng, sw, model_id=0, host_kv_fn=None, on_step=None, after_collect=False):
     """Drive the long-reasoning straggler workload: ``sw.n_live`` calls that
     arrive with a KV history are submitted up front; for the first
     ``sw.refill_steps`` steps every call that retires is replaced by a new one
     (admitted at the next step), then the batch drains. host_kv_fn(i, L) may
     return the K/V history of sequence i (None: device fill).
+    on_step(info) runs after each step is enqueued, or, with after_collect,
+    once the previous step has finished and been collected.
     Returns (tokens generated, engine steps, sequences used)."""
     nxt = 0
 
@@ -187,16 +189,20 @@ def run_straggler(eng, sw, model_id=0, host_kv_fn=None, on_step=None):
     for _ in range(sw.n_live):
         tokens += submit_one()
     steps = 0
+    first = None
     while True:
         info = eng.step()
         if info.step < 0:
             break
+        first = info.step if first is None else first
         steps += 1
-        if on_step is not None:
+        if on_step is not None and not after_collect:
             on_step(info)
-        if info.step < sw.refill_steps:
+        if info.step - first < sw.refill_steps:
             for _ in range(info.finished):
                 tokens += submit_one()
         eng.collect(info.step - 1)
+        if on_step is not None and after_collect:
+            on_step(info)
     eng.collect(-1)
     return tokens, steps, nxt

@@ -277,3 +277,17 @@ def test_straggler_workload_bookkeeping_is_bit_exact():
         assert (info.admit_step, info.finish_step) == (req.admit_step, req.finish_step)
         assert eng.block_table(req.rid) == req.blocks
     assert tokens == sum(r.G for r in s.reqs)
+
+
+def test_straggler_refill_counts_from_the_runs_first_step():
+    """A second drive of the same engine (a benchmark's timed pass after its
+    warm-up) refills for the same number of its own steps as the first."""
+    from moa_inputs import make_straggler_workload
+    from paper_2606_03014_amd.engine import run_straggler
+    c = CONFIGS["straggler-8b-bf16"]
+    sw = make_straggler_workload(0, n_live=64, refill_steps=32)
+    eng = _dry(c.model, c.engine, 1, "bf16")
+    first = run_straggler(eng, sw)
+    second = run_straggler(eng, sw)
+    assert first == second
+    assert first[2] > sw.n_live
