@@ -23,6 +23,8 @@ namespace {
 
 constexpr int kStageSlots = 4;    // steps that may be in flight (pinned staging ring)
 constexpr int kTargetWaves = 4096;
+constexpr int kBigMinRows = 256;    // a row group this large goes to the 32x32-MFMA GEMM
+constexpr int kBigTargetWgs = 256;  // one workgroup per CU
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -134,7 +136,9 @@ Layout make_layout(const moa_engine_cfg& c) {
   L.slots_cap = (int64_t)c.num_kv_blocks * kBlock / kSplitKeys + c.max_num_seqs + 1;
   L.items_cap = L.Tmax + L.slots_cap;
   L.red_cap = c.max_num_seqs;
-  int64_t pc = L.Tmax * std::max(qkv, d);
+  // split-K partials: a prefill-sized step unsplit, or a full decode batch
+  // split up to 8 ways (a few hundred rows need the split to fill the CUs)
+  int64_t pc = std::max(L.Tmax, (int64_t)8 * c.max_num_seqs) * std::max(qkv, d);
   if (c.dtype == MOA_F32) pc = std::max(pc, L.Tmax * 2 * F);
   L.part_cap = pc;
   L.token_store = c.token_store ? c.token_store : (int64_t)64 << 20;
@@ -365,6 +369,32 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     return;
   }
   const int KS = K / 32;
+  if (maxM >= kBigMinRows && N % 256 == 0) {
+    // matrix-core bound: 128-row tiles on the 32x32 MFMA, split-K only to
+    // give every CU a workgroup
+    mt = kBigTile;
+    nt = (maxM >= 1024 && N % 512 == 0) ? 4 : 2;
+    const int tiles = N / (128 * nt);
+    int base = 0;
+    for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 127) / 128) * tiles;
+    int S = 1;
+    if (allow_split)
+      while (base * S < kBigTargetWgs && KS % (S * 2) == 0 && KS / (S * 2) >= 8 &&
+             (int64_t)S * 2 * totalM * N <= e->lay.part_cap && S < 16)
+        S *= 2;
+    a.S = S;
+    a.ksteps = KS / S;
+    a.out_split = (size_t)totalM * N;
+    int item = 0;
+    for (int g = 0; g < in.ngroups; ++g) {
+      a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
+      a.g[g].n_mc = (in.nrows[g] + 127) / 128;
+      a.g[g].item0 = item;
+      item += a.g[g].n_mc * S * tiles;
+    }
+    a.total_items = item;
+    return;
+  }
   const int wmt = maxM <= 16 ? 1 : (maxM <= 32 ? 2 : 4);
   const int wnt = (maxM > 64 && N % 256 == 0) ? 4 : 2;
   const bool wg = N % (64 * wnt) == 0;

@@ -43,6 +43,10 @@ enum Epilogue { EPI_F32 = 0, EPI_SWIGLU = 1 };
 // launch_gemm(mt = kWgTile + MT, nt = NT): the workgroup-tile kernel; each item
 // is one workgroup of 16*MT rows x 64*NT columns x one k-split (N % (64*NT) == 0).
 constexpr int kWgTile = 1000;
+// launch_gemm(mt = kBigTile, nt = 2 | 4): the large-M kernel on the 32x32
+// MFMA; each item is 128 rows x 128*nt columns x one k-split
+// (N % (128*nt) == 0, K % 32 == 0, ksteps >= 1).
+constexpr int kBigTile = 2000;
 
 // Attention work item: one query row against keys [k0, k1) of its request.
 // bt_off: index in the block store of the block holding key k0 (k0 is a

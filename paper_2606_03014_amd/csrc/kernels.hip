@@ -41,6 +41,7 @@ static void klaunch(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
@@ -455,6 +456,186 @@ __global__ __launch_bounds__(256) void k_gemm_wg(GemmArgs a, int nwg) {
   }
 }
 
+// ------------------------------------------------- large-M GEMM (32x32 MFMA)
+// For row groups of a few hundred rows and up (prefill chunks, big decode
+// batches) the GEMM is bound by the matrix cores. v_mfma_f32_32x32x16_bf16
+// sustains about twice the rate of the 16x16x32 form on gfx950, so this path
+// uses it. A workgroup of WM x WN waves computes a (64 WM) x (128 WN) tile;
+// each wave owns 2 x 4 tiles of 32 x 32. Operand layout of the 32x32x16
+// MFMA: A lane l holds row l%32, k = 8 (l/32) .. +8 of a 16-wide k step; B
+// lane l holds column l%32 at the same k; accumulator element e of lane l is
+// row 8 (e/4) + 4 (l/32) + e%4, column l%32.
+//
+// Both operands reach LDS through direct global->LDS loads (no register
+// staging), one 1 KB MFMA fragment per instruction, into a ring of P stages
+// of 32 k each; stage st+P is requested while stage st is consumed, and each
+// wave waits for its own loads with an explicit vmcnt before the workgroup
+// barrier. Activations are read from the split-bf16 planes (both planes of a
+// row tile go through the same B fragment: two MFMAs); weights are read from
+// the tile-shuffled layout, whose 16-column fragments pair up into 32-column
+// MFMA tiles (SwiGLU: a gate tile and the matching up tile side by side).
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
+#define MOA_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+
+template <int WM, int WN, int EPI, int P>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) {
+  constexpr int TM = 2, TN = 4;
+  constexpr int NW = WM * WN;
+  constexpr int BM = 32 * TM * WM, BN = 32 * TN * WN;
+  constexpr int FA = (BM / 32) * 4;                   // A fragments per stage: (row tile, plane, k half)
+  constexpr int FB = (BN / 32) * 2;                   // B fragments per stage: (column tile, k half)
+  constexpr int SLOT = (FA + FB) * 1024;
+  constexpr int DPW = (FA + FB) / NW;                 // direct loads per wave per stage
+  static_assert((FA + FB) % NW == 0, "fragments per wave");
+  extern __shared__ __align__(1024) unsigned char smem[];
+  const int per = (nwg + 7) / 8;
+  const int blk = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (blk >= a.total_items) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int wm = w / WN, wn = w % WN;
+  const void* Wg = a.g[0].W;
+  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroups; ++i) {
+    if (i < a.ngroups && a.g[i].item0 <= blk) {
+      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
+    }
+  }
+  const int idx = blk - item0;
+  const int mc = idx % n_mc;
+  const int rest = idx / n_mc;
+  const int s = rest % a.S;
+  const int nb = rest / a.S;
+  const int ks0 = s * a.ksteps;
+  const int nt0 = nb * (BN / 16);                     // first 16-column weight tile of the block
+  const int KS = a.K >> 5;
+  const int rbase = row0 + mc * BM;
+  const int rend = row0 + nrows;
+  const int c = lane & 31, kh = lane >> 5;
+
+  // per-lane sources of this wave's fragments (fragment w*DPW + i of a stage)
+  const unsigned char* src[DPW];
+  int stride[DPW];
+#pragma unroll
+  for (int i = 0; i < DPW; ++i) {
+    const int f = w * DPW + i;
+    if (f < FA) {
+      const int rt = f >> 2, p = (f >> 1) & 1, h = f & 1;
+      const int r = min(rbase + 32 * rt + c, rend - 1);
+      src[i] = (const unsigned char*)((const uint16_t*)a.X + (size_t)p * a.x_lo + (size_t)r * a.K +
+                                      (size_t)ks0 * 32 + 16 * h + 8 * kh);
+      stride[i] = 64;                                 // bytes per 32-k stage
+    } else {
+      const int g = f - FA, ct = g >> 1, h = g & 1;
+      const int tw = (EPI == EPI_F32) ? nt0 + 2 * ct + (c >> 4) : nt0 + 4 * (ct >> 1) + 2 * (c >> 4) + (ct & 1);
+      src[i] = (const unsigned char*)((const u32x4*)Wg + ((size_t)tw * KS + ks0) * 64 + 16 * (2 * h + kh) + (c & 15));
+      stride[i] = 1024;
+    }
+  }
+  const int nk = a.ksteps;
+  auto issue = [&](int st) {
+    unsigned char* sl = smem + (st % P) * SLOT;
+#pragma unroll
+    for (int i = 0; i < DPW; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)st * stride[i]), MOA_LDS(sl + (w * DPW + i) * 1024),
+                                       16, 0, 0);
+  };
+  // this wave's LDS reads are complete (a wait the compiler sees), then the
+  // workgroup barrier, with no fence that would drain the direct loads
+  auto barrier = [] {
+    wait_lgkm0();
+    asm volatile("s_barrier" ::: "memory");
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+  auto load = [&](int st, int h, u32x4* ra, u32x4* rb) {
+    const unsigned char* sl = smem + (st % P) * SLOT + lane * 16;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int p = 0; p < 2; ++p) ra[i * 2 + p] = *(const u32x4*)(sl + (((wm * TM + i) * 2 + p) * 2 + h) * 1024);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) rb[j] = *(const u32x4*)(sl + (FA + (wn * TN + j) * 2 + h) * 1024);
+  };
+  auto mfmas = [&](const u32x4* ra, const u32x4* rb) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, ra[i * 2 + p]),
+                                                              __builtin_bit_cast(bf16x8_t, rb[j]), acc[i][j], 0, 0, 0);
+  };
+
+#pragma unroll
+  for (int i = 0; i < P; ++i)
+    if (i < nk) issue(i);
+  if (P <= nk) wait_vmcnt<DPW * (P - 1)>(); else wait_vmcnt<0>();
+  barrier();
+  u32x4 ra0[2 * TM], rb0[TN], ra1[2 * TM], rb1[TN];
+  load(0, 0, ra0, rb0);
+  // stage st: the second k half is read while the first is multiplied; then
+  // stage st+1 is made resident, the slot of stage st refilled with stage
+  // st+P, and the first half of st+1 read while the second half of st is
+  // multiplied. The last stage is peeled so the loop body has no join.
+  for (int st = 0; st + 1 < nk; ++st) {
+    wait_lgkm0();
+    load(st, 1, ra1, rb1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(ra0, rb0);
+    if (st + P <= nk) wait_vmcnt<DPW * (P - 2)>(); else wait_vmcnt<0>();
+    barrier();
+    if (st + P < nk) issue(st + P);
+    load(st + 1, 0, ra0, rb0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfmas(ra1, rb1);
+  }
+  load(nk - 1, 1, ra1, rb1);
+  mfmas(ra0, rb0);
+  mfmas(ra1, rb1);
+
+  const int rw = rbase + wm * TM * 32;
+  if (EPI == EPI_F32) {
+    float* out = a.out + (size_t)s * a.out_split;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int col = nt0 * 16 + (wn * TN + j) * 32 + c;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = rw + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
+          if (r < rend) out[(size_t)r * a.N + col] = acc[i][j][e];
+        }
+      }
+  } else {
+    const int half = a.N >> 1;
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int q = 0; q < TN / 2; ++q) {
+        const int hc = nt0 * 8 + ((wn * TN) / 2 + q) * 32 + c;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = rw + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
+          if (r < rend) {
+            const float g = acc[i][2 * q][e], u = acc[i][2 * q + 1][e];
+            store_split(a.hout, a.h_lo, (size_t)r * half + hc, g / (1.f + __expf(-g)) * u);
+          }
+        }
+      }
+  }
+}
+
 // ------------------------------------------------------------ fp32 GEMM
 // Plain fp32 FMA GEMM for the fp32 engine mode: a workgroup computes 16 rows
 // x 64 columns; W is row-major [N][K].
@@ -571,13 +752,15 @@ __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ part,
 // wavefront with shuffles, and P.V accumulates per lane on its own keys and
 // dims (combined once at the end). Softmax runs in base 2 on scores
 // pre-scaled by log2(e)/sqrt(hd).
-template <int HD, int GQ, bool BF>
-__global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ items, const float* __restrict__ qv,
+#ifndef ATTN_WPE
+#define ATTN_WPE 1
+#endif
+template <int HD, int GQ, bool BF, int TK>
+__global__ __launch_bounds__(GQ * 64, ATTN_WPE) void k_attn(const AttnItem* __restrict__ items, const float* __restrict__ qv,
                                                   const void* __restrict__ kvv, const int* __restrict__ bt_store,
                                                   const int* __restrict__ row_bt, int layer, int NB, int n_h,
                                                   int n_kv, float scale_log2, void* __restrict__ outv,
                                                   size_t out_lo, float* __restrict__ pacc, float* __restrict__ pml) {
-  constexpr int TK = 64;
   constexpr int CH = HD / 8;
   constexpr int ESZ = BF ? 2 : 4;
   constexpr int ROWB = HD * ESZ;
@@ -648,9 +831,10 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
     __syncthreads();
     if (t0 + TK < it.k1) fetch(t0 + TK);
 
-    float s[8];
+    constexpr int NP = TK / 8;                   // keys per lane group
+    float s[NP];
 #pragma unroll
-    for (int p8 = 0; p8 < 8; ++p8) {
+    for (int p8 = 0; p8 < NP; ++p8) {
       const int key = p8 * 8 + g8;
       float dot = 0.f;
       if (BF) {
@@ -667,7 +851,7 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
     }
     float mx = s[0];
 #pragma unroll
-    for (int p8 = 1; p8 < 8; ++p8) mx = fmaxf(mx, s[p8]);
+    for (int p8 = 1; p8 < NP; ++p8) mx = fmaxf(mx, s[p8]);
     mx = fmaxf(mx, dpp<0x128>(mx));
     mx = fmaxf(mx, swz_xor16(mx));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
@@ -677,7 +861,7 @@ __global__ __launch_bounds__(GQ * 64) void k_attn(const AttnItem* __restrict__ i
 #pragma unroll
     for (int i = 0; i < CH; ++i) acc[i] *= alpha;
 #pragma unroll
-    for (int p8 = 0; p8 < 8; ++p8) {
+    for (int p8 = 0; p8 < NP; ++p8) {
       const float pj = exp2f(s[p8] - mnew);
       l += pj;
       const int key = p8 * 8 + g8;
@@ -1079,8 +1263,29 @@ static void gemm_nt(hipStream_t st, const GemmArgs& a, int blocks, int epi, int 
   else gemm_u<MT, 1, EPI_F32>(st, a, blocks);
 }
 
+template <int WM, int WN, int P, int EPI>
+static hipError_t gemm_big(hipStream_t st, const GemmArgs& a) {
+  constexpr int BM = 64 * WM, BN = 128 * WN;
+  constexpr unsigned shm = ((BM / 32) * 4 + (BN / 32) * 2) * 1024 * P;
+  static bool attr = false;                           // one attribute call per instantiation
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<WM, WN, EPI, P>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int nwg = a.total_items;
+  klaunch_shm(k_gemm_big<WM, WN, EPI, P>, dim3((nwg + 7) / 8 * 8), dim3(64 * WM * WN), shm, st, a, nwg);
+  return hipGetLastError();
+}
+
 hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt) {
   if (a.total_items <= 0) return hipSuccess;
+  if (bf16 && mt == kBigTile) {                       // 128 x (128 nt) tiles on the 32x32 MFMA
+    if (nt == 2) return epi == EPI_SWIGLU ? gemm_big<2, 2, 4, EPI_SWIGLU>(st, a) : gemm_big<2, 2, 4, EPI_F32>(st, a);
+    if (nt == 4) return epi == EPI_SWIGLU ? gemm_big<2, 4, 3, EPI_SWIGLU>(st, a) : gemm_big<2, 4, 3, EPI_F32>(st, a);
+    return hipErrorInvalidValue;
+  }
   if (bf16 && mt >= kWgTile) {
     const int m = mt - kWgTile;          // rows / 16
     const int nwg = a.total_items;
@@ -1131,15 +1336,18 @@ hipError_t launch_rope_kv(hipStream_t st, bool bf16, const float* part, int nspl
   return hipGetLastError();
 }
 
-template <int HD, bool BF>
+#ifndef ATTN_TK64
+#define ATTN_TK64 64
+#endif
+template <int HD, bool BF, int TK = (HD == 64 && BF) ? ATTN_TK64 : 64>
 static hipError_t attn_gq(hipStream_t st, int gq, dim3 grid, unsigned shm, const AttnItem* items, const float* q,
                           const void* kv, const int* bt, const int* row_bt, int layer, int NB, int n_h, int n_kv,
                           float sl2, void* out, size_t out_lo, float* pacc, float* pml) {
   switch (gq) {
-    case 1: klaunch_shm(k_attn<HD, 1, BF>, grid, dim3(64), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 2: klaunch_shm(k_attn<HD, 2, BF>, grid, dim3(128), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 4: klaunch_shm(k_attn<HD, 4, BF>, grid, dim3(256), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
-    case 8: klaunch_shm(k_attn<HD, 8, BF>, grid, dim3(512), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 1: klaunch_shm(k_attn<HD, 1, BF, TK>, grid, dim3(64), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 2: klaunch_shm(k_attn<HD, 2, BF, TK>, grid, dim3(128), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 4: klaunch_shm(k_attn<HD, 4, BF, TK>, grid, dim3(256), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
+    case 8: klaunch_shm(k_attn<HD, 8, BF, TK>, grid, dim3(512), shm, st, items, q, kv, bt, row_bt, layer, NB, n_h, n_kv, sl2, out, out_lo, pacc, pml); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -218,3 +218,58 @@ def test_bf16_injected_history_pareto_lengths():
         flips = check_tokens(ref, toks, f"history L={L}")
         say(f"history L={L} R={R}: |engine - oracle| {err:.3e} flips {flips}")
         assert err <= 2e-2
+
+
+def test_bf16_wide_decode_batch():
+    """A decode batch of 300 rows of one 8B-width model (two layers): every
+    projection and the LM head run as one 300-row group, the shape of the
+    straggler workload's refill phase. Eight of the calls carry a host K/V
+    history and are checked teacher-forced against the oracle; the rest have
+    device-filled histories and only set the batch shape."""
+    from moa_inputs import f32_to_bf16_bits
+    from moa_inputs.workload import synthetic_kv
+    shape = replace(LLAMA_8B, n_layers=2)
+    consts = EngineConsts(num_kv_blocks=8192, max_num_seqs=512, max_prefill_tokens=64, max_model_len=1024)
+    w = generate_weights(LLAMA_8B, "bf16", 5, 4, 0, n_layers=2)
+    n, R = 300, 2
+    rng = np.random.default_rng(13)
+    Ls = [int(x) for x in rng.integers(1, 400, n)]
+    seeds = [int(x) for x in rng.integers(0, shape.vocab, n)]
+    checked = [int(x) for x in np.linspace(0, n - 1, 8).round()]
+    hist, caps, rids = {}, {}, []
+    eng = Engine(shape, "bf16", consts, 1)
+    try:
+        mid = eng.load(pack_blob(w, shape))
+        for i in range(n):
+            kvb = None
+            if i in checked:
+                kvb = f32_to_bf16_bits(synthetic_kv(1, i, 2, Ls[i], shape.n_kv_heads, shape.head_dim))
+                hist[i] = kvb
+            rid = eng.submit_with_history(mid, seeds[i], Ls[i], R, kvb)
+            rids.append(rid)
+            if i in checked:
+                caps[i] = np.full(R * shape.vocab, np.nan, dtype=np.float32)
+                eng.capture_logits(rid, caps[i])
+        steps = []
+        while True:
+            info = eng.step()
+            if info.step < 0:
+                break
+            steps.append(info.decode_rows)
+        got = {r[0]: r[3] for r in eng.collect()}
+    finally:
+        eng.close()
+    assert steps[0] == n, f"first step decoded {steps[0]} rows, want {n}"
+    om = T.OracleModel(shape, w, cache=False)
+    for i in checked:
+        toks = got[rids[i]]
+        kv = T.ContiguousKV(2, shape.n_kv_heads, shape.head_dim)
+        for layer in range(2):
+            kv.K[layer] = T.to_f64(hist[i][layer, 0])
+            kv.V[layer] = T.to_f64(hist[i][layer, 1])
+        seq = [seeds[i]] + [int(t) for t in toks[:-1]]
+        ref = T.forward_chunk(om, seq, Ls[i], kv, bf16_kv=True)
+        err = float(np.abs(caps[i].reshape(R, -1) - ref).max())
+        flips = check_tokens(ref, toks, f"wide batch seq {i}")
+        say(f"wide batch seq {i} L={Ls[i]}: |engine - oracle| {err:.3e} flips {flips}")
+        assert err <= 2e-2
