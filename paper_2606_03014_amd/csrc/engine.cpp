@@ -1052,7 +1052,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
           const int ctx = pos + 1;
           const int bto = (int)r.bt_off;
           if (a.kind == 0 && tiled_prefill) {
-            if (i % 64 == 0) e->pitems.push_back({row, pos, std::min(64, a.len - i), bto});
+            if (i % kPrefillRows == 0) e->pitems.push_back({row, pos, std::min(kPrefillRows, a.len - i), bto});
           } else if (a.kind == 0) {
             e->items.push_back({row, 0, ctx, -1, bto, 0, 0, 0});
           } else {

@@ -54,8 +54,9 @@ constexpr int kBigTile = 2000;
 struct AttnItem { int row, k0, k1, slot, bt_off, pad0, pad1, pad2; };
 struct ReduceItem { int row, slot0, nslots, pad; };
 // Causal prefill block: step rows [row0, row0 + nq) hold positions
-// [pos0, pos0 + nq) of one request (nq <= 64); keys [0, pos0 + nq).
+// [pos0, pos0 + nq) of one request (nq <= kPrefillRows); keys [0, pos0 + nq).
 // bt_off: the request's block list in the block store.
+constexpr int kPrefillRows = 128;
 struct PrefillItem { int row0, pos0, nq, bt_off; };
 
 struct StepDev {

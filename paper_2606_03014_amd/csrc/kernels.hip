@@ -46,6 +46,19 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// (a, b) -> two bf16 in one word (a low), round to nearest even: one
+// v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ unsigned pack_bf16(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2_t){a, b}, bf16x2_t));
+}
+// Split-bf16 pair: hi = bf16(a, b); lo = bf16 of the remainders.
+__device__ __forceinline__ void split_pair(float a, float b, unsigned& hi, unsigned& lo) {
+  hi = pack_bf16(a, b);
+  lo = pack_bf16(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u));
+}
+
 // fp32 -> bf16, round to nearest even (NaN stays NaN).
 __device__ __forceinline__ uint16_t f2bf(float f) {
   uint32_t u = __float_as_uint(f);
@@ -856,13 +869,13 @@ __global__ __launch_bounds__(GQ * 64, ATTN_WPE) void k_attn(const AttnItem* __re
     mx = fmaxf(mx, swz_xor16(mx));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mnew = fmaxf(m, mx);
-    const float alpha = exp2f(m - mnew);
+    const float alpha = __builtin_amdgcn_exp2f(m - mnew);
     l *= alpha;
 #pragma unroll
     for (int i = 0; i < CH; ++i) acc[i] *= alpha;
 #pragma unroll
     for (int p8 = 0; p8 < NP; ++p8) {
-      const float pj = exp2f(s[p8] - mnew);
+      const float pj = __builtin_amdgcn_exp2f(s[p8] - mnew);
       l += pj;
       const int key = p8 * 8 + g8;
       if (BF) {
@@ -909,191 +922,211 @@ __global__ __launch_bounds__(GQ * 64, ATTN_WPE) void k_attn(const AttnItem* __re
 }
 
 // ------------------------------------------ causal prefill attention (MFMA)
-// bf16 KV cache. A workgroup = one query head x a block of up to 64
-// consecutive prompt positions of one request (the rows of one prefill chunk
-// in this step); its 4 wavefronts own 16 query rows each. Keys run from 0 to
-// the block's last position in tiles of 64; per tile the workgroup stages K
-// (row-major, rows padded against bank conflicts) and V transposed (V^T:
-// head-dim rows, key columns) in LDS, and loads the next tile meanwhile.
-// Each wavefront then computes, on MFMA 16x16x32 with fp32 accumulation:
-//   S = Q K^T  (A = 16 query rows x 32 dims of q, pre-scaled by
-//               log2(e)/sqrt(hd), as split bf16 hi + lo; B = K fragments),
-// applies the causal mask and the online softmax on the fragments (an S or O
-// fragment holds rows 4*(l/16)+i of column l%16, so every row statistic
-// lives in the lanes that own that row), writes P to its own LDS slab, and
-//   O += P V   (A = P as split bf16 read back from the slab; B = V^T fragments).
+// Causal prefill attention on the 32x32x16 MFMA. A workgroup is one query
+// head and up to kPrefillRows consecutive positions of one request, four
+// wavefronts of 32 query rows each; key tiles of 32 keys cover [0, pos0 + nq).
+// Scores are formed transposed, S^T = K Q^T (A = K tile, B = the wave's q
+// rows), so lane l of a wave holds the 16 scores of query row l%32 for keys
+// 8(e/4) + 4(l/32) + e%4 of the tile: the online softmax is per lane (plus
+// one exchange with lane l^32), and those 16 probabilities are directly the
+// B operand of O^T = V^T P^T, with the key order inside each 16-key step
+// permuted identically in A (V^T, read from LDS) and B (P^T, in registers).
+// q and P enter the MFMAs as split bf16 (hi + lo, two MFMAs each). K tiles
+// reach LDS by direct global->LDS loads into a three-stage ring, in MFMA
+// fragment order; V tiles go through registers and are stored transposed.
+#ifndef PREFILL_WPE
+#define PREFILL_WPE 2
+#endif
 template <int HD>
-__global__ __launch_bounds__(256) void k_prefill_attn(const PrefillItem* __restrict__ items,
+__global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const PrefillItem* __restrict__ items,
                                                       const float* __restrict__ qv, const uint16_t* __restrict__ kv,
                                                       const int* __restrict__ bt_store, int layer, int NB, int n_h,
                                                       int n_kv, float scale_log2, uint16_t* __restrict__ out,
                                                       size_t out_lo) {
-  constexpr int TK = 64;                    // keys per tile
-  constexpr int KS = HD / 32;               // MFMA k-steps over head_dim (S = Q K^T)
-  constexpr int NT = HD / 16;               // 16-dim output tiles (O = P V)
-  constexpr int KROW = HD * 2 + 16;         // padded bytes per K row in LDS
-  constexpr int VROW = TK * 2 + 16;         // padded bytes per V^T row in LDS
-  constexpr int CPK = HD / 8;               // 16-byte chunks per key row
-  constexpr int NCH = TK * CPK;             // chunks per tile (K or V)
-  constexpr int PER = NCH / 256;            // per thread (K and V each)
-  static_assert(PER >= 1 && PER * 256 == NCH, "tile");
-  __shared__ __align__(16) unsigned char sK[TK * KROW];
-  __shared__ __align__(16) unsigned char sVt[HD * VROW];
-  __shared__ __align__(16) float sP[4][16 * TK];
+  constexpr int TK = 32;                    // keys per tile
+  constexpr int DS = HD / 16;               // 16-wide dim steps of S^T = K Q^T
+  constexpr int DT = HD / 32;               // 32-dim tiles of O^T
+  constexpr int KFR = DS;                   // K fragments (1 KB) per tile
+  constexpr int KPW = KFR / 4;              // K fragments loaded per wave
+  constexpr int NKS = 3;                    // K ring stages
+  constexpr int VROW = TK * 2 + 8;          // bytes per V^T row (padded against bank conflicts)
+  constexpr int VCH = TK * HD / 8;          // 16-byte V chunks per tile
+  constexpr int VPT = VCH / 256;            // per thread
+  static_assert(KPW >= 1 && KPW * 4 == KFR && VPT * 256 == VCH, "tile shape");
+  __shared__ __align__(1024) unsigned char sK[NKS][KFR * 1024];
+  __shared__ __align__(16) unsigned char sVt[2][HD * VROW];
 
   const PrefillItem it = items[blockIdx.x];
   const int h = blockIdx.y;
-  const int gq = n_h / n_kv;
-  const int kvh = h / gq;
+  const int kvh = h / (n_h / n_kv);
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int c32 = lane & 31, hf = lane >> 5;
   const int kmax = it.pos0 + it.nq;          // keys [0, kmax)
+  const int ntile = (kmax + TK - 1) / TK;
   const size_t hs = (size_t)2 * kBlock * HD;
   const uint16_t* pool = kv + ((size_t)layer * NB * n_kv + kvh) * hs;
   const size_t bstride = (size_t)n_kv * hs;
   const int* bt = bt_store + it.bt_off;
 
-  // q fragments for this wavefront's 16 rows (rows past nq read row nq-1: never stored)
-  u32x4 qh[KS], ql[KS];
+  // B operand of S^T: query row 32w + l%32 (rows past nq read row nq-1 and
+  // are never stored), dims 16s + 8(l/32) .. +8, scaled to log2 units, split
+  u32x4 qh[DS], ql[DS];
   {
-    const int r = min(16 * w + (lane & 15), it.nq - 1);
-    const float* qrow = qv + ((size_t)(it.row0 + r) * n_h + h) * HD;
+    const int r = min(32 * w + c32, it.nq - 1);
+    const float* qrow = qv + ((size_t)(it.row0 + r) * n_h + h) * HD + 8 * hf;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
+    for (int s = 0; s < DS; ++s) {
       unsigned hv[4], lv[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float x0 = qrow[ks * 32 + (lane >> 4) * 8 + 2 * j] * scale_log2;
-        const float x1 = qrow[ks * 32 + (lane >> 4) * 8 + 2 * j + 1] * scale_log2;
-        const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
-        hv[j] = (unsigned)h0 | ((unsigned)h1 << 16);
-        lv[j] = (unsigned)f2bf(x0 - bf2f(h0)) | ((unsigned)f2bf(x1 - bf2f(h1)) << 16);
-      }
-      qh[ks] = u32x4{hv[0], hv[1], hv[2], hv[3]};
-      ql[ks] = u32x4{lv[0], lv[1], lv[2], lv[3]};
+      for (int j = 0; j < 4; ++j)
+        split_pair(qrow[16 * s + 2 * j] * scale_log2, qrow[16 * s + 2 * j + 1] * scale_log2, hv[j], lv[j]);
+      qh[s] = u32x4{hv[0], hv[1], hv[2], hv[3]};
+      ql[s] = u32x4{lv[0], lv[1], lv[2], lv[3]};
     }
   }
-  f32x4_t O[NT];
-#pragma unroll
-  for (int n = 0; n < NT; ++n) O[n] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m[4], l[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) { m[i] = -INFINITY; l[i] = 0.f; }
-  const int kl = lane & 15, rq = (lane >> 4) * 4;
+  const int qpos = it.pos0 + 32 * w + c32;   // this lane's query position
 
-  u32x4 kc[PER], vc[PER];
-  auto fetch = [&](int t0) {
+  // K tile t: fragment s holds key t*32 + l%32, dims 16s + 8(l/32) .. +8 in lane l
+  auto issue_k = [&](int t) {
+    const int key = min(t * TK + c32, kmax - 1);
+    const uint16_t* base = pool + (size_t)bt[key >> 4] * bstride + (key & 15) * HD + 8 * hf;
+    unsigned char* sl = sK[t % NKS];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
+    for (int i = 0; i < KPW; ++i) {
+      const int s = w * KPW + i;
+      __builtin_amdgcn_global_load_lds((const void*)(base + 16 * s), MOA_LDS(sl + s * 1024), 16, 0, 0);
+    }
+  };
+  // V chunk c of a tile: key c % 32 (adjacent lanes hold adjacent keys), dims
+  // 8 (c / 32) .. +8
+  u32x4 vr[VPT];
+  auto load_v = [&](int t) {
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
       const int c = threadIdx.x + 256 * j;
-      const int key = c / CPK, cc = c - key * CPK;
-      const int p = t0 + key;
-      kc[j] = u32x4{0u, 0u, 0u, 0u};
-      vc[j] = u32x4{0u, 0u, 0u, 0u};
-      if (p < kmax) {
-        const uint16_t* base = pool + (size_t)bt[p >> 4] * bstride + (p & 15) * HD + cc * 8;
-        kc[j] = *(const u32x4*)base;
-        vc[j] = *(const u32x4*)(base + kBlock * HD);
+      const int key = min(t * TK + (c & 31), kmax - 1), cc = c >> 5;
+      vr[j] = *(const u32x4*)(pool + (size_t)bt[key >> 4] * bstride + kBlock * HD + (key & 15) * HD + cc * 8);
+    }
+  };
+  // V^T: row = dim, keys contiguous. The lanes of an even/odd key pair swap
+  // their chunks (one DPP move per word); the even lane then writes dims 0..3
+  // and the odd lane dims 4..7 of the chunk, each as (even key, odd key) words.
+  auto store_vt = [&](int t) {
+    unsigned char* vt = sVt[t & 1];
+    const bool odd = lane & 1;
+#pragma unroll
+    for (int j = 0; j < VPT; ++j) {
+      const int c = threadIdx.x + 256 * j;
+      const int k2 = (c & 31) & ~1, cc = c >> 5;
+      unsigned pw[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) pw[e] = (unsigned)__builtin_amdgcn_mov_dpp((int)vr[j][e], 0xB1, 0xF, 0xF, true);
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const unsigned mine = vr[j][odd ? e + 2 : e], other = pw[odd ? e + 2 : e];
+        const unsigned ev = odd ? other : mine, od = odd ? mine : other;   // even-key word, odd-key word
+        const int dim = cc * 8 + (odd ? 4 : 0) + 2 * e;
+        *(unsigned*)(vt + dim * VROW + k2 * 2) = (ev & 0xffffu) | (od << 16);
+        *(unsigned*)(vt + (dim + 1) * VROW + k2 * 2) = (ev >> 16) | (od & 0xffff0000u);
       }
     }
   };
-  fetch(0);
-  for (int t0 = 0; t0 < kmax; t0 += TK) {
-    __syncthreads();                                    // previous tile's LDS reads are done
+  auto barrier = [] {
+    wait_lgkm0();
+    asm volatile("s_barrier" ::: "memory");
+  };
+
+  f32x16_t O[DT];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int c = threadIdx.x + 256 * j;
-      const int key = c / CPK, cc = c - key * CPK;
-      *(u32x4*)(sK + key * KROW + cc * 16) = kc[j];
+  for (int d = 0; d < DT; ++d) O[d] = f32x16_t{};
+  float m = -INFINITY, l = 0.f;
+
+  // prologue: K tiles 0 and 1 requested, V^T of tile 0 stored, V of tile 1 in registers
+  issue_k(0);
+  if (ntile > 1) issue_k(1);
+  load_v(0);
+  store_vt(0);
+  if (ntile > 1) load_v(1);
+  for (int t = 0; t < ntile; ++t) {
+    // K tile t landed (loads issued after it: K(t+1) and V(t+1), when they exist)
+    if (t + 1 < ntile) wait_vmcnt<KPW + VPT>(); else wait_vmcnt<0>();
+    barrier();                               // K(t), V^T(t) visible; slots of t-1 free
+    if (t + 2 < ntile) issue_k(t + 2);
+    const unsigned char* sl = sK[t % NKS] + lane * 16;
+    // two independent accumulation chains (q hi, q lo) keep the MFMA pipe busy
+    f32x16_t S = f32x16_t{}, S2 = f32x16_t{};
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {                     // V^T: element (dim, key)
-        const unsigned wv = vc[j][e];
-        *(uint16_t*)(sVt + (cc * 8 + 2 * e) * VROW + key * 2) = (uint16_t)(wv & 0xffffu);
-        *(uint16_t*)(sVt + (cc * 8 + 2 * e + 1) * VROW + key * 2) = (uint16_t)(wv >> 16);
+    for (int s = 0; s < DS; ++s) {
+      const u32x4 ka = *(const u32x4*)(sl + s * 1024);
+      S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, ka), __builtin_bit_cast(bf16x8_t, qh[s]), S, 0, 0, 0);
+      S2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, ka), __builtin_bit_cast(bf16x8_t, ql[s]), S2, 0, 0, 0);
+    }
+    S += S2;
+    // causal mask (only tiles that reach past the wave's first query or past
+    // kmax need it) and online softmax for query qpos (element e: key kb +
+    // 8(e/4) + e%4)
+    const int kb = t * TK + 4 * hf;
+    if (t * TK + TK - 1 > it.pos0 + 32 * w || t * TK + TK > kmax) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int key = kb + 8 * (e >> 2) + (e & 3);
+        if (key > qpos || key >= kmax) S[e] = -INFINITY;
       }
     }
-    __syncthreads();
-    if (t0 + TK < kmax) fetch(t0 + TK);
-    // S = Q K^T for the 4 key groups of the tile
-    f32x4_t S[4];
+    float mx = S[0];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      S[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int e = 1; e < 16; ++e) mx = fmaxf(mx, S[e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    const float base = (mn == -INFINITY) ? 0.f : mn;   // a row with no key yet keeps m = -inf
+    const float alpha = __builtin_amdgcn_exp2f(m - base);
+    float ts = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const u32x4 kb = *(const u32x4*)(sK + (16 * g + kl) * KROW + (ks * 32 + (lane >> 4) * 8) * 2);
-        S[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, qh[ks]),
-                                                       __builtin_bit_cast(bf16x8_t, kb), S[g], 0, 0, 0);
-        S[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ql[ks]),
-                                                       __builtin_bit_cast(bf16x8_t, kb), S[g], 0, 0, 0);
-      }
+    for (int e = 0; e < 16; ++e) {
+      S[e] = __builtin_amdgcn_exp2f(S[e] - base);
+      ts += S[e];
     }
-    // causal mask + online softmax; this lane owns rows rq+i (positions pos0 + 16w + rq + i)
-    float alpha[4];
+    ts += __shfl_xor(ts, 32, 64);
+    l = l * alpha + ts;
+    m = mn;
+    if (!__all(alpha == 1.f)) {                // no row's maximum moved: nothing to rescale
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int qpos = it.pos0 + 16 * w + rq + i;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int key = t0 + 16 * g + kl;
-        if (key > qpos || key >= kmax) S[g][i] = -INFINITY;
-        mx = fmaxf(mx, S[g][i]);
-      }
-      mx = max16(mx);
-      const float mn = fmaxf(m[i], mx);
-      // a row with no key yet (only possible for rows past nq) keeps m = -inf
-      const float base = (mn == -INFINITY) ? 0.f : mn;
-      alpha[i] = exp2f(m[i] - base);
-      float ts = 0.f;
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const float pj = exp2f(S[g][i] - base);
-        ts += pj;
-        sP[w][(rq + i) * TK + 16 * g + kl] = pj;
-      }
-      ts = sum16(ts);
-      l[i] = l[i] * alpha[i] + ts;
-      m[i] = mn;
+      for (int d = 0; d < DT; ++d) O[d] *= alpha;
     }
+    // O^T += V^T P^T over two 16-key steps; slot j of step u is key 16u + 8(j/4) + 4(l/32) + j%4
+    const unsigned char* vt = sVt[t & 1];
 #pragma unroll
-    for (int n = 0; n < NT; ++n)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) O[n][i] *= alpha[i];
-    wave_lds_fence();
-    // O += P V over two 32-key k-steps
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const float* pr = &sP[w][kl * TK + ks * 32 + (lane >> 4) * 8];
+    for (int u = 0; u < 2; ++u) {
       unsigned ph[4], pl[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float x0 = pr[2 * j], x1 = pr[2 * j + 1];
-        const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
-        ph[j] = (unsigned)h0 | ((unsigned)h1 << 16);
-        pl[j] = (unsigned)f2bf(x0 - bf2f(h0)) | ((unsigned)f2bf(x1 - bf2f(h1)) << 16);
-      }
+      for (int j = 0; j < 4; ++j) split_pair(S[8 * u + 2 * j], S[8 * u + 2 * j + 1], ph[j], pl[j]);
       const u32x4 pa = u32x4{ph[0], ph[1], ph[2], ph[3]}, pb = u32x4{pl[0], pl[1], pl[2], pl[3]};
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const u32x4 vb = *(const u32x4*)(sVt + (16 * n + kl) * VROW + (ks * 32 + (lane >> 4) * 8) * 2);
-        O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, pa),
-                                                       __builtin_bit_cast(bf16x8_t, vb), O[n], 0, 0, 0);
-        O[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, pb),
-                                                       __builtin_bit_cast(bf16x8_t, vb), O[n], 0, 0, 0);
+      for (int d = 0; d < DT; ++d) {
+        const unsigned char* row = vt + (32 * d + c32) * VROW;
+        const uint2 v0 = *(const uint2*)(row + (16 * u + 4 * hf) * 2);
+        const uint2 v1 = *(const uint2*)(row + (16 * u + 8 + 4 * hf) * 2);
+        const u32x4 va = u32x4{v0.x, v0.y, v1.x, v1.y};
+        O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va), __builtin_bit_cast(bf16x8_t, pa), O[d], 0, 0, 0);
+        O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va), __builtin_bit_cast(bf16x8_t, pb), O[d], 0, 0, 0);
       }
     }
-    wave_lds_fence();
-  }
-  // normalise and store rows < nq (O fragment: row rq+i, dim 16n + kl)
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = 16 * w + rq + i;
-    if (r < it.nq) {
-      const float inv = 1.f / l[i];
-      const size_t o = ((size_t)(it.row0 + r) * n_h + h) * HD + kl;
-#pragma unroll
-      for (int n = 0; n < NT; ++n) store_split(out, out_lo, o + 16 * n, O[n][i] * inv);
+    // V^T of tile t+1 into the other buffer (its last readers passed this
+    // iteration's barrier), then V of tile t+2 into registers
+    if (t + 1 < ntile) {
+      store_vt(t + 1);
+      if (t + 2 < ntile) load_v(t + 2);
     }
+  }
+  // normalise and store: element e of O[d] is dim 32d + 8(e/4) + 4(l/32) + e%4 of row 32w + l%32
+  const int r = 32 * w + c32;
+  if (r < it.nq) {
+    const float inv = 1.f / l;
+    const size_t o = ((size_t)(it.row0 + r) * n_h + h) * HD + 4 * hf;
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) store_split(out, out_lo, o + 32 * d + 8 * (e >> 2) + (e & 3), O[d][e] * inv);
   }
 }
 
