@@ -219,11 +219,16 @@ def bench_feeder(args, cfg, eng, mids):
         phase["decode_rows"] += info.decode_rows
         phase["prefill_steps"] += 1 if info.prefill_tokens else 0
 
+    gate = {}
+    if args.gate_tau is not None:
+        A = args.answer_options
+        gate = dict(gate_tau=args.gate_tau, answer_of=lambda q, e, toks: int(toks[0]) % A)
+
     def one_step():
         prog.reset()
         for k in phase:
             phase[k] = 0
-        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step)
+        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step, order=args.order, **gate)
 
     for i in range(args.warmup):
         t = time.perf_counter()
@@ -234,6 +239,7 @@ def bench_feeder(args, cfg, eng, mids):
     torch.cuda.synchronize()
     tokens = steps = prefill_tokens = 0
     t0 = time.perf_counter()
+    r = None
     for i in range(args.steps):
         r = one_step()
         tokens += r.tokens
@@ -248,7 +254,12 @@ def bench_feeder(args, cfg, eng, mids):
               "prefill_tokens_per_step": prefill_tokens // args.steps,
               "engine_steps_per_step": steps // args.steps, "seed": args.seed,
               "parallelism": "single GPU"}
-    extra = {"prefill_tokens_per_s": prefill_tokens / wall}
+    extra = {"prefill_tokens_per_s": prefill_tokens / wall, "makespan_s": wall / args.steps}
+    if cfg.aggregator:
+        extra["aggregation"] = {"aggregator_calls": r.agg_calls, "skipped_by_gate": len(r.gated),
+                                "gate_tau": args.gate_tau, "answer_options": args.answer_options if gate else None,
+                                "answer": "first generated token mod answer_options" if gate else None}
+    config["order"] = args.order
     return tokens, wall, config, extra, wl
 
 
@@ -324,6 +335,12 @@ def main():
     ap.add_argument("--time-every", type=int, default=8, help="time the kernels of 1 step in N")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--gate-tau", type=float, default=None,
+                    help="adaptive-aggregation gate threshold (skip the aggregator when the experts' vote share >= tau)")
+    ap.add_argument("--answer-options", type=int, default=4,
+                    help="synthetic answer space of the gate: an expert's answer is its first token mod this")
+    ap.add_argument("--order", default="first-seen", choices=["first-seen", "longest-first"],
+                    help="submission order of the expert calls")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 8 times (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -357,6 +374,8 @@ def main():
     stats = eng.kernel_stats()
     roof = kernel_summary(stats)
     run_roof_ms = sum(s["roof_ms_all"] for s in stats.values())
+    # kernel time of every launch, estimated from the timed sample of each class
+    busy_ms = sum(s["ms"] / s["launches"] * s["launches_all"] for s in stats.values() if s["launches"])
 
     out = {
         "metric": METRIC,
@@ -374,7 +393,8 @@ def main():
         "config": config,
         "roofline": roof,
         "run_roofline": {"roof_ms": run_roof_ms / args.steps, "measured_ms": wall * 1e3 / args.steps,
-                         "frac": run_roof_ms / (wall * 1e3)},
+                         "frac": run_roof_ms / (wall * 1e3),
+                         "kernel_ms_est": busy_ms / args.steps, "gpu_busy_frac": busy_ms / (wall * 1e3)},
         "kernel_classes": class_rates(stats),
     }
     out.update(extra)

@@ -162,15 +162,28 @@ class OracleScheduler:
         return out
 
 
+def c_vote(answers):
+    """Plurality fraction of the adaptive-aggregation gate (Section "MOSAIC:
+    Adaptive Aggregation", Eq. 11 and Algorithm 1): the largest number of
+    experts that gave one same answer, divided by the number of experts k."""
+    from collections import Counter
+    from fractions import Fraction
+    return Fraction(max(Counter(answers).values()), len(answers))
+
+
 def run_feeder(sched, expert_calls, agg_model=-1, agg_G=0, query_len=None,
-               query_experts=None, direct_calls=()):
+               query_experts=None, direct_calls=(), gate_tau=None, answers=None):
     """Drive ``sched`` the way the engine's feeder drives the engine.
 
     expert_calls: [(q, e, P, G)] in first-seen order. direct_calls: [(q, model,
     P, G)] submitted up front after the expert calls (no experts to wait for).
     Aggregator calls have prompt length query_len[q] + sum of the G of its
     experts. Returns (collect_log, rid_of) with collect_log a list of
-    (after_step, [rids]) and rid_of[(q, model)] -> rid."""
+    (after_step, [rids]) and rid_of[(q, model)] -> rid.
+
+    gate_tau: Algorithm 1's threshold. When a query's experts are all done,
+    its aggregator call is made only if c_vote of answers[(q, e)] over its
+    experts is below gate_tau; otherwise no call (the majority answer stands)."""
     rid_of = {}
     for q, e, P, G in expert_calls:
         rid_of[(q, e)] = sched.submit(e, P, G)
@@ -201,6 +214,11 @@ def run_feeder(sched, expert_calls, agg_model=-1, agg_G=0, query_len=None,
                 if remaining[q] == 0:
                     ready.append(q)
         for q in sorted(ready):
+            if gate_tau is not None:
+                from fractions import Fraction
+                if c_vote([answers[(q, e)] for e in query_experts[q]]) >= Fraction(gate_tau).limit_denominator(64):
+                    del remaining[q]
+                    continue
             rid = sched.submit(agg_model, query_len[q] + gsum[q], agg_G)
             rid_of[(q, agg_model)] = rid
             by_rid[rid] = (q, agg_model)

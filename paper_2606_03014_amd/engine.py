@@ -9,6 +9,8 @@ each step, collects what retired one step earlier and submits the aggregator
 call of every query whose experts are all done (ascending query id), on
 query ++ outputs in ascending expert order.
 """
+from fractions import Fraction
+
 import numpy as np
 
 from . import moa as M
@@ -106,17 +108,53 @@ class FeedResult:
         self.collects = []       # (after_step, [request ids])
         self.n_steps = 0
         self.tokens = 0
+        self.gated = {}          # q -> majority answer, for queries whose aggregator call the gate skipped
+        self.agg_calls = 0       # aggregator calls submitted
 
 
-def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None):
+def plurality(answers):
+    """Confidence of a set of expert answers as in the adaptive-aggregation
+    gate (Eq. 11): the share of the most frequent answer among the k answers,
+    as an exact fraction, and that answer (the smallest one if several tie)."""
+    counts = {}
+    for a in answers:
+        counts[a] = counts.get(a, 0) + 1
+    top = max(counts.values())
+    return Fraction(top, len(answers)), min(a for a, c in counts.items() if c == top)
+
+
+def expert_order(workload, order):
+    """Expert calls (q, e, G) in submission order. "first-seen": queries
+    ascending, experts ascending. "longest-first": largest max_new_tokens
+    first (ties in first-seen order) -- with every call's generation length
+    known up front, a longest-processing-time order starts the calls that
+    set the makespan before the short ones."""
+    calls = list(workload.expert_requests())
+    if order == "first-seen":
+        return calls
+    if order == "longest-first":
+        return sorted(calls, key=lambda c: -c[2])
+    raise ValueError(order)
+
+
+def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None,
+               gate_tau=None, answer_of=None, order="first-seen"):
     """Drive ``eng`` through ``workload`` (a moa_inputs.Workload).
 
     expert_models[e] is the engine model id of expert e; agg_model is the
     aggregator's model id (-1: none). A workload without experts sends every
-    query straight to the aggregator."""
+    query straight to the aggregator.
+
+    gate_tau: the confidence gate of the adaptive aggregation (Eq. 11,
+    Algorithm 1). When the last expert of a query finishes, its answers
+    answer_of(q, e, tokens) (experts ascending) are scored by plurality();
+    if the score is >= gate_tau the aggregator call is skipped and the
+    majority answer recorded in FeedResult.gated, else the aggregator call
+    is submitted as usual. order: see expert_order()."""
     res = FeedResult()
     who = {}
-    for q, e, G in workload.expert_requests():
+    tau = None if gate_tau is None else Fraction(gate_tau).limit_denominator(64)
+    for q, e, G in expert_order(workload, order):
         rid = eng.submit(workload.prompts[q], expert_models[e], G)
         res.rid_of[(q, expert_models[e])] = rid
         who[rid] = (q, expert_models[e], e)
@@ -126,6 +164,7 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
             rid = eng.submit(workload.prompts[q], agg_model, workload.agg_max_new)
             res.rid_of[(q, agg_model)] = rid
             who[rid] = (q, agg_model, -1)
+            res.agg_calls += 1
 
     def handle(done, after):
         if done:
@@ -140,11 +179,18 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
                 if remaining[q] == 0:
                     ready.append(q)
         for q in sorted(ready):
+            del remaining[q]
+            if tau is not None:
+                conf, majority = plurality([answer_of(q, e, res.outputs[(q, expert_models[e])])
+                                            for e in workload.experts[q]])
+                if conf >= tau:
+                    res.gated[q] = majority
+                    continue
             parts = [workload.prompts[q]] + [res.outputs[(q, expert_models[e])] for e in workload.experts[q]]
             rid = eng.submit(np.concatenate(parts).astype(np.int32), agg_model, workload.agg_max_new)
             res.rid_of[(q, agg_model)] = rid
             who[rid] = (q, agg_model, -1)
-            del remaining[q]
+            res.agg_calls += 1
         return len(ready)
 
     last = -1

@@ -81,6 +81,44 @@ def test_tiny_workload_full_fp32():
     say(f"tiny workload: {len(r.outputs)} calls checked, {nflip} near-tie flips")
 
 
+def test_tiny_workload_gated_aggregation_fp32():
+    """The tiny workload with the adaptive-aggregation gate (tau = 1): a
+    query's answer is its expert's first generated token modulo 2; queries
+    whose two experts agree skip the aggregator. The skipped set must be the
+    one the oracle's own greedy outputs give, and every call that runs must
+    match the oracle."""
+    from oracle.scheduler import c_vote
+    c = CONFIGS["tiny-moa-fp32"]
+    ws = [generate_weights(c.model, "f32", 0, c.wid, m) for m in range(3)]
+    wl = make_workload(c.name, 0)
+    eng = Engine(c.model, "f32", c.engine, 3)
+    mids = [eng.load(pack_blob(w, c.model)) for w in ws]
+    say("tiny gated workload: running")
+    r = run_feeder(eng, wl, mids[:2], agg_model=mids[2], gate_tau=1,
+                   answer_of=lambda q, e, toks: int(toks[0]) % 2)
+    eng.close()
+    models = [T.OracleModel(c.model, w) for w in ws]
+    skipped = set()
+    for q in range(wl.n_queries):
+        outs = []
+        for e in wl.experts[q]:
+            got = r.outputs[(q, mids[e])]
+            assert len(got) == wl.max_new[(q, e)]
+            check_tokens(T.teacher_forced_logits(models[e], wl.prompts[q], got), got, f"q{q} expert {e}")
+            outs.append(int(got[0]) % 2)
+        if c_vote(outs) >= 1:                 # the gate re-derived from the oracle-checked outputs
+            skipped.add(q)
+    assert set(r.gated) == skipped
+    assert 0 < len(skipped) < wl.n_queries
+    for q in range(wl.n_queries):
+        assert ((q, mids[2]) in r.outputs) == (q not in skipped)
+        if q not in skipped:
+            prompt = np.concatenate([wl.prompts[q]] + [r.outputs[(q, mids[e])] for e in wl.experts[q]])
+            toks = r.outputs[(q, mids[2])]
+            check_tokens(T.teacher_forced_logits(models[2], prompt, toks), toks, f"agg q{q}")
+    say(f"tiny gated workload: {len(skipped)} of {wl.n_queries} aggregator calls skipped")
+
+
 def test_tiny_logits_fp32_chunked_and_split():
     """fp32 logits within 1e-4 on prompts that span several prefill chunks
     (budget 64) and contexts past one 256-key decode split."""
