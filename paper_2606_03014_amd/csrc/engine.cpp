@@ -413,9 +413,16 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     target = kTargetWaves;
   }
   for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + rows_per - 1) / rows_per) * tiles;
+  // split-K granularity and target, from weight-streaming sweeps with cold
+  // weights: deep-K projections (K >= 4N) stream best with half the
+  // workgroups (longer k runs per workgroup); square ones at <= 8 rows with
+  // twice as many (k runs of 4 stages)
+  int kmul = 8;
+  if (wg && K >= 4 * N) target /= 2;
+  else if (wg && K == N && maxM <= 8) { target *= 2; kmul = 4; }
   int S = 1;
   if (allow_split) {
-    while (base * S < target && KS % (S * 2 * 8) == 0 &&
+    while (base * S < target && KS % (S * 2 * kmul) == 0 &&
            (int64_t)S * 2 * totalM * N <= e->lay.part_cap && S < 16)
       S *= 2;
   }

@@ -1320,6 +1320,7 @@ hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, in
     return hipErrorInvalidValue;
   }
   if (bf16 && mt >= kWgTile) {
+    if (a.ksteps % 4 != 0) return hipErrorInvalidValue;   // the kernel consumes k in stages of 4 steps
     const int m = mt - kWgTile;          // rows / 16
     const int nwg = a.total_items;
     const int grid = (nwg + 7) / 8 * 8;
