@@ -373,7 +373,7 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     // matrix-core bound: 128-row tiles on the 32x32 MFMA, split-K only to
     // give every CU a workgroup
     mt = kBigTile;
-    nt = (maxM >= 1024 && N % 512 == 0) ? 4 : 2;
+    nt = (maxM >= 512 && N % 512 == 0) ? 4 : 2;      // 128 x 512 tiles once there are rows for them
     const int tiles = N / (128 * nt);
     int base = 0;
     for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 127) / 128) * tiles;
