@@ -369,6 +369,8 @@ def main():
     eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models)
     log(f"[bench] {cfg.name}: {n_models} model(s); arena {eng.arena_bytes / 2**30:.1f} GiB")
     mids, weights0 = load_models(eng, cfg, args.seed, n_models)
+    read_bps, mfma_fps = eng.measure_peaks()
+    log(f"[bench] measured peaks: HBM read {read_bps / 1e12:.2f} TB/s, bf16 32x32x16 MFMA {mfma_fps / 1e15:.2f} PFLOP/s")
     run = bench_straggler if straggler else bench_feeder
     tokens, wall, config, extra, wl = run(args, cfg, eng, mids)
     stats = eng.kernel_stats()
@@ -396,6 +398,12 @@ def main():
                          "frac": run_roof_ms / (wall * 1e3),
                          "kernel_ms_est": busy_ms / args.steps, "gpu_busy_frac": busy_ms / (wall * 1e3)},
         "kernel_classes": class_rates(stats),
+        # the same roofline against what this GPU sustains (per kernel class:
+        # max(bytes / measured read bandwidth, useful flops / measured MFMA rate))
+        "measured_peaks": {"hbm_read_GBps": read_bps / 1e9, "mfma_bf16_TFLOPs": mfma_fps / 1e12},
+        "run_roofline_measured_peaks": {
+            "roof_ms": sum(max(s["bytes_all"] / read_bps, s["flops_all"] / mfma_fps) for s in stats.values()) * 1e3 / args.steps,
+            "frac": sum(max(s["bytes_all"] / read_bps, s["flops_all"] / mfma_fps) for s in stats.values()) / wall},
     }
     out.update(extra)
     eng.close()

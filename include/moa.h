@@ -241,6 +241,16 @@ moa_status moa_debug_time_kernels(moa_engine* e, int32_t every, double peak_bw, 
 /* Statistics per class, out[MOA_K_COUNT]. Waits for the stream. */
 moa_status moa_debug_kernel_stats(moa_engine* e, moa_kernel_stats* out);
 
+/* What this GPU sustains, measured on the engine's stream (the device work
+ * runs now; the call returns when it is done): *read_bytes_per_s = streaming
+ * HBM read bandwidth over up to 8 GiB of the KV pool (read only; the pool must
+ * be at least 1 GiB), *mfma_flops_per_s = bf16 matrix-core throughput of the
+ * 32x32x16 MFMA (dense, 2*32*32*16 flops per instruction). Each is the best of
+ * five timed runs after a warm-up. Uses the logits workspace as scratch
+ * (overwritten; call between steps). EINVAL: null outputs or a pool under
+ * 1 GiB; ESTATE: plan-only engine or unusable engine; EHIP: runtime error. */
+moa_status moa_debug_measure_peaks(moa_engine* e, double* read_bytes_per_s, double* mfma_flops_per_s);
+
 #ifdef __cplusplus
 }
 #endif

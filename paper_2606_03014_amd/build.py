@@ -9,7 +9,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libmoa.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["engine.cpp", "kernels.hip"]
+SOURCES = ["engine.cpp", "kernels.hip", "peaks.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # keep the compiler from forming packed fp32 ops on this target
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -1275,6 +1275,40 @@ moa_status moa_debug_kernel_stats(moa_engine* e, moa_kernel_stats* out) {
   return MOA_OK;
 }
 
+moa_status moa_debug_measure_peaks(moa_engine* e, double* read_bytes_per_s, double* mfma_flops_per_s) {
+  if (!e || !read_bytes_per_s || !mfma_flops_per_s) return MOA_EINVAL;
+  if (e->broken || e->plan_only) return MOA_ESTATE;
+  const size_t bytes = std::min(e->lay.kv_bytes, (size_t)8 << 30) & ~(size_t)15;
+  if (bytes < ((size_t)1 << 30)) return MOA_EINVAL;
+  const size_t sink_bytes = (size_t)e->lay.Rmax * e->cfg.model.vocab * 4;
+  const int read_grid = 4096, mfma_grid = 1024, iters = 8192;   // ~2 ms per MFMA run
+  if (sink_bytes < (size_t)mfma_grid * 256 * 4 || sink_bytes < (size_t)read_grid * 4) return MOA_EINVAL;
+  hipEvent_t a = nullptr, b = nullptr;
+  HIPCHK(hipEventCreate(&a), "peaks event");
+  HIPCHK(hipEventCreate(&b), "peaks event");
+  double best_read = 0, best_mfma = 0;
+  for (int rep = 0; rep < 6; ++rep) {
+    float ms = 0.f;
+    HIPCHK(hipEventRecord(a, e->stream), "peaks event");
+    HIPCHK(launch_peak_read(e->stream, e->kv, bytes, (unsigned*)e->logits, read_grid), "peak read");
+    HIPCHK(hipEventRecord(b, e->stream), "peaks event");
+    HIPCHK(hipEventSynchronize(b), "peaks wait");
+    HIPCHK(hipEventElapsedTime(&ms, a, b), "peaks time");
+    if (rep > 0 && ms > 0) best_read = std::max(best_read, bytes / (ms * 1e-3));
+    HIPCHK(hipEventRecord(a, e->stream), "peaks event");
+    HIPCHK(launch_peak_mfma(e->stream, e->logits, mfma_grid, iters), "peak mfma");
+    HIPCHK(hipEventRecord(b, e->stream), "peaks event");
+    HIPCHK(hipEventSynchronize(b), "peaks wait");
+    HIPCHK(hipEventElapsedTime(&ms, a, b), "peaks time");
+    if (rep > 0 && ms > 0) best_mfma = std::max(best_mfma, (double)mfma_grid * 4 * iters * 4 * 32768.0 / (ms * 1e-3));
+  }
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+  *read_bytes_per_s = best_read;
+  *mfma_flops_per_s = best_mfma;
+  return MOA_OK;
+}
+
 moa_status moa_debug_capture_logits(moa_engine* e, int64_t id, float* host_logits) {
   if (!e || !host_logits || id < 0 || id >= (int64_t)e->reqs.size()) return MOA_EINVAL;
   Request& r = e->reqs[id];

@@ -119,4 +119,10 @@ hipError_t launch_kv_fill(hipStream_t st, bool bf16, void* kv, const int* blocks
 hipError_t launch_argmax(hipStream_t st, const float* logits, int R, int V, const int* lm_dst,
                          int* tok_store);
 
+// Peak microbenchmarks (peaks.hip). read: every byte of [p, p + bytes) once;
+// sink needs `grid` words. mfma: grid workgroups of 4 waves, 4 * iters
+// 32x32x16 bf16 MFMAs per wave; sink needs grid * 256 floats.
+hipError_t launch_peak_read(hipStream_t st, const void* p, size_t bytes, unsigned* sink, int grid);
+hipError_t launch_peak_mfma(hipStream_t st, float* sink, int grid, int iters);
+
 }  // namespace moa

@@ -85,6 +85,9 @@ class Engine:
     def kernel_stats(self):
         return M.moa_debug_kernel_stats(self.h)
 
+    def measure_peaks(self):
+        return M.moa_debug_measure_peaks(self.h)
+
     def capture_logits(self, rid, arr):
         M.moa_debug_capture_logits(self.h, rid, arr)
 

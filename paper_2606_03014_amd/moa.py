@@ -78,6 +78,7 @@ _SIGS = {
     "moa_debug_capture_logits": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_float)]),
     "moa_debug_time_kernels": (C.c_int, [C.c_void_p, C.c_int32, C.c_double, C.c_double]),
     "moa_debug_kernel_stats": (C.c_int, [C.c_void_p, P(moa_kernel_stats)]),
+    "moa_debug_measure_peaks": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double)]),
 }
 
 _lib = None
@@ -259,3 +260,10 @@ def moa_debug_kernel_stats(eng):
     check(lib().moa_debug_kernel_stats(eng, out), "moa_debug_kernel_stats")
     return {n: {f: getattr(out[i], f) for f, _ in moa_kernel_stats._fields_}
             for i, n in enumerate(KERNEL_CLASSES)}
+
+
+def moa_debug_measure_peaks(eng):
+    """(HBM read bytes/s, bf16 32x32x16 MFMA flop/s) measured on the engine's stream."""
+    r, f = C.c_double(), C.c_double()
+    check(lib().moa_debug_measure_peaks(eng, C.byref(r), C.byref(f)), "moa_debug_measure_peaks")
+    return r.value, f.value

@@ -246,12 +246,13 @@ def test_hand_traced_injected_history_matches():
 
 
 def test_straggler_workload_bookkeeping_is_bit_exact():
-    """Refill phase (every retired call replaced at the next admission) then
-    drain, against the oracle scheduler driven the same way."""
+    """The whole straggler workload -- refill phase (every retired call
+    replaced at the next admission) then drain -- against the oracle
+    scheduler driven the same way."""
     from moa_inputs import make_straggler_workload
     from paper_2606_03014_amd.engine import run_straggler
     c = CONFIGS["straggler-8b-bf16"]
-    sw = make_straggler_workload(0, n_live=512, refill_steps=64)
+    sw = make_straggler_workload(0)                   # the whole workload: 512 live, 512 refill steps
     eng = _dry(c.model, c.engine, 1, "bf16")
     tokens, steps, used = run_straggler(eng, sw)
     s = OracleScheduler(c.engine.num_kv_blocks, c.engine.max_num_seqs, c.engine.max_prefill_tokens, 1,
