@@ -324,6 +324,62 @@ def bench_straggler(args, cfg, eng, mids):
     return tokens, wall, config, {"phases": phases}, None
 
 
+def calibrate_placement(args, cfg):
+    """Fit the session model T = t_step * O^max + t_token * N * Obar on this
+    engine from three timed single-model sessions, then solve the placement
+    ILP (Eq. 4-10) for the workload's experts on 1..8 workers (capacity 2),
+    with the measured model-load time as l_m. Prints one JSON line."""
+    import numpy as np
+    import torch
+    from moa_inputs import make_workload
+    from paper_2606_03014_amd import Engine
+    from paper_2606_03014_amd.placement import (ModelCost, fit_session_model, output_stats,
+                                                session_time, solve_placement)
+    from moa_inputs import generate_weights, pack_blob
+    eng = Engine(cfg.model, cfg.dtype, cfg.engine, 1)
+    blob = pack_blob(generate_weights(cfg.model, cfg.dtype, args.seed, cfg.wid, 0, threads=16), cfg.model)
+    torch.cuda.synchronize()
+    t = time.perf_counter()                    # l_m: host weights -> a ready expert on the GPU
+    mids = [eng.load(blob)]
+    torch.cuda.synchronize()
+    load_s = time.perf_counter() - t
+    del blob
+    rng = np.random.default_rng([args.seed, 91])
+    samples = []
+    for n, G, P in ((8, 256, 128), (64, 128, 128), (16, 1024, 128)):
+        prompts = [rng.integers(0, cfg.model.vocab, P).astype(np.int32) for _ in range(n)]
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for pr in prompts:
+            eng.submit(pr, mids[0], G)
+        while eng.step().step >= 0:
+            pass
+        eng.collect(-1)
+        torch.cuda.synchronize()
+        samples.append((n, float(G), float(G), time.perf_counter() - t))
+        log(f"[bench] calibration session: {n} calls x {G} tokens in {samples[-1][3]:.2f} s")
+    eng.close()
+    t_step, t_token = fit_session_model(samples)
+    wl = make_workload(cfg.name, args.seed, n_queries=args.queries)
+    models = []
+    for e in range(cfg.n_experts):
+        lens = [G for (q, ee, G) in wl.expert_requests() if ee == e]
+        om, ox = output_stats(lens)
+        models.append(ModelCost(f"expert{e}", len(lens), load_s, session_time(len(lens), om, ox, t_step, t_token)))
+    plans = {}
+    for N in range(1, 9):
+        try:
+            p = solve_placement(models, N, 2)
+            plans[N] = {"makespan_s": p.makespan, "Y": p.Y.tolist(), "X": p.X.tolist(), "replica_caps": p.caps}
+        except ValueError as err:
+            plans[N] = {"infeasible": str(err)}
+    print(json.dumps({"calibration": {"t_step_s": t_step, "t_token_s": t_token, "load_s": load_s,
+                                      "sessions": samples},
+                      "experts": [{"name": m.name, "N_m": m.n_prompts, "T_hat_s": m.T_hat, "tau_s": m.tau}
+                                  for m in models],
+                      "placements_K2": plans, "workload": cfg.name}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -341,6 +397,8 @@ def main():
                     help="synthetic answer space of the gate: an expert's answer is its first token mod this")
     ap.add_argument("--order", default="first-seen", choices=["first-seen", "longest-first"],
                     help="submission order of the expert calls")
+    ap.add_argument("--calibrate-placement", action="store_true",
+                    help="fit the per-model session cost on this engine and solve the placement ILP for 1..8 workers")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 8 times (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -364,6 +422,9 @@ def main():
     from paper_2606_03014_amd import Engine
 
     cfg = CONFIGS[args.workload]
+    if args.calibrate_placement:
+        calibrate_placement(args, cfg)
+        return
     straggler = cfg.name.startswith("straggler")
     n_models = cfg.n_experts + (1 if cfg.aggregator else 0)
     eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models)
