@@ -783,7 +783,7 @@ __global__ __launch_bounds__(GQ * 64, ATTN_WPE) void k_attn(const AttnItem* __re
   constexpr int PER = (NCH + NT - 1) / NT;       // chunks per thread
   __shared__ __align__(16) unsigned char sK[TK * ROWB];
   __shared__ __align__(16) unsigned char sV[TK * ROWB];
-  extern __shared__ int sbt[];                   // block ids of the key range
+  extern __shared__ unsigned long long sbo[];    // byte offsets of the key range's blocks in the layer's pool
 
   const AttnItem it = items[blockIdx.x];
   const int kvh = blockIdx.y;
@@ -791,56 +791,66 @@ __global__ __launch_bounds__(GQ * 64, ATTN_WPE) void k_attn(const AttnItem* __re
   const int g8 = lane >> 3, c8 = lane & 7;
   const int h = kvh * GQ + w;
 
+  const size_t hs = (size_t)2 * kBlock * HD;     // elements per (block, kv head)
+  const unsigned char* pool = (const unsigned char*)kvv + ((size_t)layer * NB * n_kv + kvh) * hs * ESZ;
+  const unsigned long long blk_stride = (unsigned long long)n_kv * hs * ESZ;
   const int b0 = it.k0 >> 4, nb = ((it.k1 - 1) >> 4) - b0 + 1;
   {
     const int* bt = bt_store + it.bt_off;
-    for (int i = threadIdx.x; i < nb; i += NT) sbt[i] = bt[i];
+    for (int i = threadIdx.x; i < nb; i += NT) sbo[i] = (unsigned long long)bt[i] * blk_stride;
   }
-  float q[CH];
+  // bf16 cache: q enters the dot products as a split-bf16 pair (hi + lo,
+  // pre-scaled by log2(e)/sqrt(hd)) through v_dot2_f32_bf16, which multiplies
+  // bf16 pairs exactly and accumulates in fp32; fp32 cache: plain fp32 q.
+  float q[BF ? 1 : CH];
+  unsigned qh[BF ? CH / 2 : 1], ql[BF ? CH / 2 : 1];
   {
     const size_t qo = ((size_t)it.row * n_h + h) * HD + c8 * CH;
+    if (BF) {
 #pragma unroll
-    for (int i = 0; i < CH; ++i) q[i] = qv[qo + i];
+      for (int i = 0; i < CH / 2; ++i)
+        split_pair(qv[qo + 2 * i] * scale_log2, qv[qo + 2 * i + 1] * scale_log2, qh[i], ql[i]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < CH; ++i) q[i] = qv[qo + i];
+    }
   }
   float m = -INFINITY, l = 0.f, acc[CH];
 #pragma unroll
   for (int i = 0; i < CH; ++i) acc[i] = 0.f;
-  __syncthreads();
 
-  const size_t hs = (size_t)2 * kBlock * HD;     // elements per (block, kv head)
-  const unsigned char* pool = (const unsigned char*)kvv + ((size_t)layer * NB * n_kv + kvh) * hs * ESZ;
-  const size_t blk_stride = (size_t)n_kv * hs * ESZ;
+  // loop-invariant part of every chunk this thread moves: key in the tile,
+  // byte offset inside its 16-slot block, LDS destination
+  int ckey[PER];
+  unsigned coff[PER];
+  unsigned char* cdst[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int c = min((int)threadIdx.x + j * NT, NCH - 1);
+    const int isV = c / (TK * CPR);
+    const int rem = c - isV * (TK * CPR);
+    const int key = rem / CPR, cc = rem - key * CPR;
+    ckey[j] = (threadIdx.x + j * NT < NCH) ? key : (1 << 29);     // out-of-tile chunks never load
+    coff[j] = (unsigned)((isV * kBlock * HD + (key & 15) * HD) * ESZ + cc * 16);
+    cdst[j] = (isV ? sV : sK) + rem * 16;
+  }
+  __syncthreads();
 
   uint4 pre[PER];
   auto fetch = [&](int t0) {
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-      const int c = threadIdx.x + j * NT;
+      const int p = t0 + ckey[j];
       uint4 val = make_uint4(0u, 0u, 0u, 0u);
-      if (c < NCH) {
-        const int isV = c / (TK * CPR);
-        const int rem = c - isV * (TK * CPR);
-        const int key = rem / CPR, cc = rem - key * CPR;
-        const int p = t0 + key;
-        if (p < it.k1) {
-          const int blk = sbt[(p >> 4) - b0];
-          val = *(const uint4*)(pool + blk * blk_stride + ((size_t)isV * kBlock * HD + (p & 15) * HD) * ESZ + cc * 16);
-        }
-      }
+      if (p < it.k1) val = *(const uint4*)(pool + sbo[(p >> 4) - b0] + coff[j]);
       pre[j] = val;
     }
   };
   fetch(it.k0);
   for (int t0 = it.k0; t0 < it.k1; t0 += TK) {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-      const int c = threadIdx.x + j * NT;
-      if (c < NCH) {
-        const int isV = c / (TK * CPR);
-        const int rem = c - isV * (TK * CPR);
-        *(uint4*)((isV ? sV : sK) + rem * 16) = pre[j];
-      }
-    }
+    for (int j = 0; j < PER; ++j)
+      if (threadIdx.x + j * NT < NCH) *(uint4*)cdst[j] = pre[j];
     __syncthreads();
     if (t0 + TK < it.k1) fetch(t0 + TK);
 
@@ -851,16 +861,21 @@ __global__ __launch_bounds__(GQ * 64, ATTN_WPE) void k_attn(const AttnItem* __re
       const int key = p8 * 8 + g8;
       float dot = 0.f;
       if (BF) {
-        const uint16_t* kr = (const uint16_t*)(sK + key * ROWB) + c8 * CH;
+        const unsigned* kr = (const unsigned*)(sK + key * ROWB + c8 * CH * 2);
 #pragma unroll
-        for (int i = 0; i < CH; ++i) dot = fmaf(q[i], bf2f(kr[i]), dot);
+        for (int i = 0; i < CH / 2; ++i) {
+          const bf16x2_t kp = __builtin_bit_cast(bf16x2_t, kr[i]);
+          dot = __builtin_amdgcn_fdot2_f32_bf16(kp, __builtin_bit_cast(bf16x2_t, qh[i]), dot, false);
+          dot = __builtin_amdgcn_fdot2_f32_bf16(kp, __builtin_bit_cast(bf16x2_t, ql[i]), dot, false);
+        }
+        dot = sum8(dot);
       } else {
         const float* kr = (const float*)(sK + key * ROWB) + c8 * CH;
 #pragma unroll
         for (int i = 0; i < CH; ++i) dot = fmaf(q[i], kr[i], dot);
+        dot = sum8(dot) * scale_log2;
       }
-      dot = sum8(dot);
-      s[p8] = (t0 + key < it.k1) ? dot * scale_log2 : -INFINITY;
+      s[p8] = (t0 + key < it.k1) ? dot : -INFINITY;
     }
     float mx = s[0];
 #pragma unroll
@@ -1393,7 +1408,7 @@ hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, in
                             void* out, size_t out_lo, float* pacc, float* pml) {
   if (nitems <= 0) return hipSuccess;
 
-  const unsigned shm = (unsigned)max_item_blocks * 4u;
+  const unsigned shm = (unsigned)max_item_blocks * 8u;   // one 64-bit block offset per block of an item
   if (shm > 48u * 1024u) return hipErrorInvalidValue;
   const int gq = n_h / n_kv;
   const float sl2 = scale * 1.4426950408889634f;
