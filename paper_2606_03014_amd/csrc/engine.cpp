@@ -1087,6 +1087,12 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
     }
   }
   const int R = (int)e->l_src.size();
+  // Launch order of the decode-attention items: full-length key ranges first,
+  // then the shorter ones by decreasing length, so the grid ends on its
+  // shortest workgroups. Every item writes its own partial slot (or its row's
+  // output), so the order changes no result.
+  std::stable_sort(e->items.begin(), e->items.end(),
+                   [](const AttnItem& a, const AttnItem& b) { return a.k1 - a.k0 > b.k1 - b.k0; });
   if (!e->plan_only) {
     if (T > e->lay.Tmax || R > e->lay.Rmax || nslots > e->lay.slots_cap ||
         (int64_t)e->items.size() > e->lay.items_cap) {
