@@ -28,6 +28,12 @@ sys.path.insert(0, ROOT)
 HBM_PEAK = 8.0e12            # bytes/s, MI355X HBM3E
 MFMA_BF16_PEAK = 2.5e15      # flop/s, dense bf16
 METRIC = "generated tokens/s on 1 MI355X (ragged MoA batch); attn/GEMM % of HBM/MFMA roof"
+# per-step cost model of the schedule study: the decode streaming rate and
+# the useful prefill rates this engine reaches on 8B shapes (large-M GEMM,
+# causal prefill attention)
+STUDY_BW = 5.0e12
+STUDY_LIN = 4.7e14
+STUDY_ATTN = 3.2e14
 
 
 def log(msg):
@@ -228,7 +234,8 @@ def bench_feeder(args, cfg, eng, mids):
         prog.reset()
         for k in phase:
             phase[k] = 0
-        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step, order=args.order, **gate)
+        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step, order=args.order,
+                          window=args.window, **gate)
 
     for i in range(args.warmup):
         t = time.perf_counter()
@@ -260,6 +267,8 @@ def bench_feeder(args, cfg, eng, mids):
                                 "gate_tau": args.gate_tau, "answer_options": args.answer_options if gate else None,
                                 "answer": "first generated token mod answer_options" if gate else None}
     config["order"] = args.order
+    if args.window is not None:
+        config["window"] = args.window
     return tokens, wall, config, extra, wl
 
 
@@ -380,6 +389,71 @@ def calibrate_placement(args, cfg):
                       "placements_K2": plans, "workload": cfg.name}), flush=True)
 
 
+def schedule_study(args, cfg):
+    """Plan-only schedules of the workload under the feeder's policies
+    (submission order x submission window x prefill budget), with no GPU: the
+    engine's own scheduler plans every step, and a per-step cost model prices
+    it. Per step: the weights of every model with a row in the step at
+    STUDY_BW, the K/V of every decode row's context at STUDY_BW, prefill
+    tokens at the measured large-M GEMM rate and causal prefill pairs at the
+    measured prefill-attention rate. Prints one JSON line."""
+    import dataclasses
+    import numpy as np
+    from moa_inputs import make_workload
+    from moa_inputs.weights import tensor_shapes
+    from paper_2606_03014_amd import Engine, run_feeder
+    g = cfg.model
+    esz = 2 if cfg.dtype == "bf16" else 4
+    n_params = sum(int(np.prod(sh)) for _, sh in tensor_shapes(g))
+    streamed = (n_params - g.vocab * g.d_model) * esz           # every matrix but the embedding
+    kv_per_ctx = 2 * g.n_layers * g.n_kv_heads * g.head_dim * esz
+    lin_flops = 2.0 * (n_params - g.vocab * g.d_model)           # per prefill token
+    pair_flops = 4.0 * g.n_heads * g.head_dim * g.n_layers       # per causal (q, k) pair
+    wl = make_workload(cfg.name, args.seed, n_queries=args.queries)
+    nm = cfg.n_experts + (1 if cfg.aggregator else 0)
+    blob = np.zeros(n_params * esz, np.uint8)
+    rows_out = []
+    for order in ("first-seen", "longest-first"):
+        for window in (None, 256, 64, 16):
+            for budget in (4096, 16384, 32768):
+                consts = dataclasses.replace(cfg.engine, max_prefill_tokens=budget)
+                eng = Engine(g, cfg.dtype, consts, nm, plan_only=True)
+                for _ in range(nm):
+                    eng.load(blob)
+                r = run_feeder(eng, wl, list(range(cfg.n_experts)), agg_model=cfg.n_experts if cfg.aggregator else -1,
+                               order=order, window=window)
+                S = r.n_steps
+                active = np.zeros((S + 1, nm), bool)
+                ctx = np.zeros(S + 1)
+                pre = np.zeros(S + 1)
+                pairs = 0.0
+                gen = 0
+                for (q, m), rid in r.rid_of.items():
+                    info = eng.request(rid)
+                    ch = eng.chunks(rid)
+                    for s, a, b in ch:
+                        pre[s] += b
+                        pairs += b * a + b * (b + 1) / 2
+                        active[s, m] = True
+                    d0 = max(s for s, a, b in ch) + 1       # decode steps d0..finish, at positions P..P+G-2
+                    d1 = info.finish_step
+                    if d1 >= d0:
+                        active[d0:d1 + 1, m] = True
+                        ctx[d0:d1 + 1] += info.prompt_len + 1 + np.arange(d1 - d0 + 1)
+                    gen += info.max_new_tokens
+                t = (active.sum(axis=1) * streamed + ctx * kv_per_ctx) / STUDY_BW + pre * lin_flops / STUDY_LIN
+                model_s = float(t.sum() + pairs * pair_flops / STUDY_ATTN)
+                eng.close()
+                rows_out.append({"order": order, "window": window, "prefill_budget": budget, "steps": S,
+                                 "model_s": float(f"{model_s:.4g}"), "model_tokens_per_s": round(gen / model_s),
+                                 "mean_active_models": round(float(active[:S].sum(axis=1).mean()), 3)})
+                log(f"[bench] {order:13s} window {str(window):5s} budget {budget:6d}: {S} steps, "
+                    f"model {model_s:.1f} s")
+    print(json.dumps({"schedule_study": rows_out, "workload": cfg.name, "queries": wl.n_queries,
+                      "cost_model": {"stream_Bps": STUDY_BW, "prefill_linear_flops": STUDY_LIN,
+                                     "prefill_attention_flops": STUDY_ATTN}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -399,6 +473,11 @@ def main():
                     help="submission order of the expert calls")
     ap.add_argument("--calibrate-placement", action="store_true",
                     help="fit the per-model session cost on this engine and solve the placement ILP for 1..8 workers")
+    ap.add_argument("--schedule-study", action="store_true",
+                    help="plan-only schedules under each submission order, window and prefill budget, "
+                         "priced by a per-step cost model (no GPU)")
+    ap.add_argument("--window", type=int, default=None,
+                    help="submission window of the feeder (default: every expert call up front)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 8 times (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -411,6 +490,10 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_probe_bytes": n, "copies": 8}))
+        return
+    if args.schedule_study:
+        from moa_inputs import CONFIGS
+        schedule_study(args, CONFIGS[args.workload])
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "

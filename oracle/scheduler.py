@@ -172,7 +172,7 @@ def c_vote(answers):
 
 
 def run_feeder(sched, expert_calls, agg_model=-1, agg_G=0, query_len=None,
-               query_experts=None, direct_calls=(), gate_tau=None, answers=None):
+               query_experts=None, direct_calls=(), gate_tau=None, answers=None, window=None):
     """Drive ``sched`` the way the engine's feeder drives the engine.
 
     expert_calls: [(q, e, P, G)] in first-seen order. direct_calls: [(q, model,
@@ -183,10 +183,30 @@ def run_feeder(sched, expert_calls, agg_model=-1, agg_G=0, query_len=None,
 
     gate_tau: Algorithm 1's threshold. When a query's experts are all done,
     its aggregator call is made only if c_vote of answers[(q, e)] over its
-    experts is below gate_tau; otherwise no call (the majority answer stands)."""
+    experts is below gate_tau; otherwise no call (the majority answer stands).
+
+    window: None submits every expert call up front; an integer W submits
+    the next expert calls (in the given order) only while fewer than W
+    requests wait in the scheduler's pending queue, checked after every step
+    once that step's collect has been handled (aggregator calls are submitted
+    when ready, whatever the queue holds)."""
     rid_of = {}
-    for q, e, P, G in expert_calls:
-        rid_of[(q, e)] = sched.submit(e, P, G)
+    calls = list(expert_calls)
+    nxt = [0]
+
+    def top_up():
+        n = 0
+        while nxt[0] < len(calls) and (window is None or len(sched.pending) < window):
+            q, e, P, G = calls[nxt[0]]
+            nxt[0] += 1
+            rid = sched.submit(e, P, G)
+            rid_of[(q, e)] = rid
+            by_rid[rid] = (q, e)
+            n += 1
+        return n
+
+    by_rid = {}
+    top_up()
     for q, mdl, P, G in direct_calls:
         rid_of[(q, mdl)] = sched.submit(mdl, P, G)
     remaining = {}
@@ -196,7 +216,6 @@ def run_feeder(sched, expert_calls, agg_model=-1, agg_G=0, query_len=None,
             if ex:
                 remaining[q] = len(ex)
                 gsum[q] = 0
-    by_rid = {}
     for (q, m), rid in rid_of.items():
         by_rid[rid] = (q, m)
     log = []
@@ -229,10 +248,12 @@ def run_feeder(sched, expert_calls, agg_model=-1, agg_G=0, query_len=None,
         s = sched.step()
         if s is None:
             n = handle(sched.collect(last), last)
-            if n == 0 and sched.idle():
+            m = top_up()
+            if n == 0 and m == 0 and sched.idle():
                 break
             continue
         last = s
         if s >= 1:
             handle(sched.collect(s - 1), s - 1)
+        top_up()
     return log, rid_of

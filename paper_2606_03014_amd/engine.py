@@ -141,7 +141,7 @@ def expert_order(workload, order):
 
 
 def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None,
-               gate_tau=None, answer_of=None, order="first-seen"):
+               gate_tau=None, answer_of=None, order="first-seen", window=None):
     """Drive ``eng`` through ``workload`` (a moa_inputs.Workload).
 
     expert_models[e] is the engine model id of expert e; agg_model is the
@@ -153,14 +153,37 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
     answer_of(q, e, tokens) (experts ascending) are scored by plurality();
     if the score is >= gate_tau the aggregator call is skipped and the
     majority answer recorded in FeedResult.gated, else the aggregator call
-    is submitted as usual. order: see expert_order()."""
+    is submitted as usual. order: see expert_order().
+
+    window: None submits every expert call up front. An integer W keeps at
+    most W submitted-but-unadmitted calls in the engine: expert calls are
+    submitted as admissions make room, while aggregator calls are submitted
+    the moment their experts finish, so they overtake the expert calls not
+    yet submitted (aggregation fills the gaps of the expert tail instead of
+    queueing behind every expert call)."""
     res = FeedResult()
     who = {}
     tau = None if gate_tau is None else Fraction(gate_tau).limit_denominator(64)
-    for q, e, G in expert_order(workload, order):
-        rid = eng.submit(workload.prompts[q], expert_models[e], G)
-        res.rid_of[(q, expert_models[e])] = rid
-        who[rid] = (q, expert_models[e], e)
+    if window is not None and window < 1:
+        raise ValueError("window must be >= 1")
+    queue = list(expert_order(workload, order))
+    nxt = 0
+    submitted = admitted = 0
+
+    def top_up():
+        nonlocal nxt, submitted
+        n = 0
+        while nxt < len(queue) and (window is None or submitted - admitted < window):
+            q, e, G = queue[nxt]
+            nxt += 1
+            rid = eng.submit(workload.prompts[q], expert_models[e], G)
+            res.rid_of[(q, expert_models[e])] = rid
+            who[rid] = (q, expert_models[e], e)
+            submitted += 1
+            n += 1
+        return n
+
+    top_up()
     remaining = {q: len(ex) for q, ex in enumerate(workload.experts) if ex} if agg_model >= 0 else {}
     if agg_model >= 0 and workload.n_experts == 0:
         for q in range(workload.n_queries):
@@ -168,8 +191,10 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
             res.rid_of[(q, agg_model)] = rid
             who[rid] = (q, agg_model, -1)
             res.agg_calls += 1
+            submitted += 1
 
     def handle(done, after):
+        nonlocal submitted
         if done:
             res.collects.append((after, [d[0] for d in done]))
         ready = []
@@ -194,6 +219,7 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
             res.rid_of[(q, agg_model)] = rid
             who[rid] = (q, agg_model, -1)
             res.agg_calls += 1
+            submitted += 1
         return len(ready)
 
     last = -1
@@ -201,15 +227,18 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
         info = eng.step()
         if info.step < 0:
             n = handle(eng.collect(last), last)
-            if n == 0:
+            m = top_up()
+            if n == 0 and m == 0:
                 break
             continue
         last = info.step
+        admitted += info.admitted
         res.n_steps += 1
         if on_step is not None:
             on_step(info)
         if last >= 1:
             handle(eng.collect(last - 1), last - 1)
+        top_up()
         if max_steps is not None and res.n_steps >= max_steps:
             break
     return res
