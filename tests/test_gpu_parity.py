@@ -258,18 +258,21 @@ def test_bf16_injected_history_pareto_lengths():
         assert err <= 2e-2
 
 
-def test_bf16_wide_decode_batch():
-    """A decode batch of 300 rows of one 8B-width model (two layers): every
-    projection and the LM head run as one 300-row group, the shape of the
-    straggler workload's refill phase. Eight of the calls carry a host K/V
-    history and are checked teacher-forced against the oracle; the rest have
-    device-filled histories and only set the batch shape."""
+@pytest.mark.parametrize("n", [100, 300], ids=["100-rows", "300-rows"])
+def test_bf16_wide_decode_batch(n):
+    """A decode batch of n rows of one 8B-width model (two layers): every
+    projection and the LM head run as one n-row group. 300 rows take the
+    large-M 32x32-MFMA GEMM (the shape of the straggler workload's refill
+    phase), 100 rows the workgroup-tile kernel with its widest tiles (64 rows
+    x 256 columns). Eight of the calls carry a host K/V history and are
+    checked teacher-forced against the oracle; the rest have device-filled
+    histories and only set the batch shape."""
     from moa_inputs import f32_to_bf16_bits
     from moa_inputs.workload import synthetic_kv
     shape = replace(LLAMA_8B, n_layers=2)
     consts = EngineConsts(num_kv_blocks=8192, max_num_seqs=512, max_prefill_tokens=64, max_model_len=1024)
     w = generate_weights(LLAMA_8B, "bf16", 5, 4, 0, n_layers=2)
-    n, R = 300, 2
+    R = 2
     rng = np.random.default_rng(13)
     Ls = [int(x) for x in rng.integers(1, 400, n)]
     seeds = [int(x) for x in rng.integers(0, shape.vocab, n)]
