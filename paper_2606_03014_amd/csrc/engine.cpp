@@ -875,8 +875,10 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   }
   // causal prefill blocks: K/V of keys [0, pos0 + nq) once per KV head; q.k and p.v per (row, key <= pos)
   double pre_keys = 0, pre_pairs = 0, pre_rows = 0;
+  int pre_max_keys = 1;
   for (const PrefillItem& pi : e->pitems) {
     pre_keys += pi.pos0 + pi.nq;
+    pre_max_keys = std::max(pre_max_keys, pi.pos0 + pi.nq);
     pre_pairs += (double)pi.nq * pi.pos0 + (double)pi.nq * (pi.nq + 1) / 2;
     pre_rows += pi.nq;
   }
@@ -909,7 +911,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
                             e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd, T), "rope kv");
       if (npre > 0)
         LAUNCH(MOA_K_PREFILL_ATTN, pre_bytes, pre_flops,
-               launch_prefill_attention(s, sd.pre, npre, e->q, e->kv, e->bt_store, l, e->cfg.num_kv_blocks, nh, nkv,
+               launch_prefill_attention(s, sd.pre, npre, pre_max_keys, e->q, e->kv, e->bt_store, l, e->cfg.num_kv_blocks, nh, nkv,
                                         hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo), "prefill attention");
       if (nitems > 0)
         LAUNCH(MOA_K_ATTN, attn_bytes, attn_flops,

@@ -99,9 +99,12 @@ hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, in
                             void* out, size_t out_lo, float* pacc, float* pml);
 
 // bf16 KV only, head_dim 64 or 128; writes split-bf16 rows of `out`.
-hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, int nitems, const float* q,
-                                   const void* kv, const int* bt_store, int layer, int num_blocks, int n_h,
-                                   int n_kv, int hd, float scale, void* out, size_t out_lo);
+// max_keys: the largest pos0 + nq over the items (their block lists are
+// staged in LDS; hipErrorInvalidValue when they do not fit, past ~400k keys).
+constexpr unsigned kPrefillLdsMax = 144u * 1024u;
+hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, int nitems, int max_keys,
+                                   const float* q, const void* kv, const int* bt_store, int layer, int num_blocks,
+                                   int n_h, int n_kv, int hd, float scale, void* out, size_t out_lo);
 
 hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, int nred,
                               const float* pacc, const float* pml, void* out, size_t out_lo, int n_h,

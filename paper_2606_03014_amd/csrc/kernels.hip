@@ -492,6 +492,25 @@ template <int N> __device__ __forceinline__ void wait_vmcnt() {
 }
 __device__ __forceinline__ void wait_lgkm0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 #define MOA_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+// 32-bit LDS address of a pointer into shared memory
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(size_t)(const __attribute__((address_space(3))) void*)p;
+}
+// Two 8-byte LDS reads at addr + 8*O0 and addr + 8*O1 into one register
+// quad. The compiler does not track it: pair it with lgkm_wait_for().
+template <int O0, int O1>
+__device__ __forceinline__ u32x4 ds_read2_b64(unsigned addr) {
+  u32x4 v;
+  asm volatile("ds_read2_b64 %0, %1 offset0:%2 offset1:%3" : "=v"(v) : "v"(addr), "i"(O0), "i"(O1));
+  return v;
+}
+// One 4-byte LDS store the compiler does not track (ordered by "memory" and by
+// the explicit LDS waits before each barrier).
+__device__ __forceinline__ void ds_write_b32(unsigned addr, unsigned v) {
+  asm volatile("ds_write_b32 %0, %1" : : "v"(addr), "v"(v) : "memory");
+}
+// Wait for every outstanding LDS access; tying v makes its later uses follow.
+__device__ __forceinline__ void lgkm_wait_for(u32x4& v) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v)); }
 
 template <int WM, int WN, int EPI, int P>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) {
@@ -968,8 +987,13 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   constexpr int VCH = TK * HD / 8;          // 16-byte V chunks per tile
   constexpr int VPT = VCH / 256;            // per thread
   static_assert(KPW >= 1 && KPW * 4 == KFR && VPT * 256 == VCH, "tile shape");
-  __shared__ __align__(1024) unsigned char sK[NKS][KFR * 1024];
-  __shared__ __align__(16) unsigned char sVt[2][HD * VROW];
+  // One dynamic LDS block (sized by the launcher): the K ring (NKS x KFR KB),
+  // the two V^T buffers, then the block ids of keys [0, kmax). Keeping all
+  // three in one object lets the explicit waits below order the direct loads
+  // into the ring against the V^T reads.
+  extern __shared__ __align__(1024) unsigned char sKd[];
+  unsigned char* sVt0 = sKd + NKS * KFR * 1024;
+  int* sbt = (int*)(sVt0 + 2 * HD * VROW);
 
   const PrefillItem it = items[blockIdx.x];
   const int h = blockIdx.y;
@@ -981,7 +1005,15 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   const size_t hs = (size_t)2 * kBlock * HD;
   const uint16_t* pool = kv + ((size_t)layer * NB * n_kv + kvh) * hs;
   const size_t bstride = (size_t)n_kv * hs;
-  const int* bt = bt_store + it.bt_off;
+  // The block ids live in LDS for the whole item: a K/V address then never
+  // waits on a global load, which (vector loads complete in order) would also
+  // wait for every tile already in flight.
+  {
+    const int* bt = bt_store + it.bt_off;
+    const int nblk = (kmax + kBlock - 1) / kBlock;
+    for (int i = threadIdx.x; i < nblk; i += 256) sbt[i] = bt[i];
+    __syncthreads();
+  }
 
   // B operand of S^T: query row 32w + l%32 (rows past nq read row nq-1 and
   // are never stored), dims 16s + 8(l/32) .. +8, scaled to log2 units, split
@@ -1004,8 +1036,8 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   // K tile t: fragment s holds key t*32 + l%32, dims 16s + 8(l/32) .. +8 in lane l
   auto issue_k = [&](int t) {
     const int key = min(t * TK + c32, kmax - 1);
-    const uint16_t* base = pool + (size_t)bt[key >> 4] * bstride + (key & 15) * HD + 8 * hf;
-    unsigned char* sl = sK[t % NKS];
+    const uint16_t* base = pool + (size_t)sbt[key >> 4] * bstride + (key & 15) * HD + 8 * hf;
+    unsigned char* sl = (sKd + (t % NKS) * KFR * 1024);
 #pragma unroll
     for (int i = 0; i < KPW; ++i) {
       const int s = w * KPW + i;
@@ -1020,14 +1052,17 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
     for (int j = 0; j < VPT; ++j) {
       const int c = threadIdx.x + 256 * j;
       const int key = min(t * TK + (c & 31), kmax - 1), cc = c >> 5;
-      vr[j] = *(const u32x4*)(pool + (size_t)bt[key >> 4] * bstride + kBlock * HD + (key & 15) * HD + cc * 8);
+      vr[j] = *(const u32x4*)(pool + (size_t)sbt[key >> 4] * bstride + kBlock * HD + (key & 15) * HD + cc * 8);
     }
   };
   // V^T: row = dim, keys contiguous. The lanes of an even/odd key pair swap
   // their chunks (one DPP move per word); the even lane then writes dims 0..3
   // and the odd lane dims 4..7 of the chunk, each as (even key, odd key) words.
+  // The stores are explicit LDS instructions, like the V^T reads: the
+  // compiler would otherwise hold each of them until the direct loads into
+  // the K ring have landed.
   auto store_vt = [&](int t) {
-    unsigned char* vt = sVt[t & 1];
+    const unsigned vt = lds_addr(sVt0 + (t & 1) * HD * VROW);
     const bool odd = lane & 1;
 #pragma unroll
     for (int j = 0; j < VPT; ++j) {
@@ -1036,13 +1071,16 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
       unsigned pw[4];
 #pragma unroll
       for (int e = 0; e < 4; ++e) pw[e] = (unsigned)__builtin_amdgcn_mov_dpp((int)vr[j][e], 0xB1, 0xF, 0xF, true);
+      // the even lane keeps words 0-1 (dims 0..3), the odd lane words 2-3 (dims 4..7)
+      const unsigned mine0 = odd ? vr[j][2] : vr[j][0], mine1 = odd ? vr[j][3] : vr[j][1];
+      const unsigned oth0 = odd ? pw[2] : pw[0], oth1 = odd ? pw[3] : pw[1];
+      const unsigned base = vt + (cc * 8 + (odd ? 4 : 0)) * VROW + k2 * 2;
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const unsigned mine = vr[j][odd ? e + 2 : e], other = pw[odd ? e + 2 : e];
+        const unsigned mine = e ? mine1 : mine0, other = e ? oth1 : oth0;
         const unsigned ev = odd ? other : mine, od = odd ? mine : other;   // even-key word, odd-key word
-        const int dim = cc * 8 + (odd ? 4 : 0) + 2 * e;
-        *(unsigned*)(vt + dim * VROW + k2 * 2) = (ev & 0xffffu) | (od << 16);
-        *(unsigned*)(vt + (dim + 1) * VROW + k2 * 2) = (ev >> 16) | (od & 0xffff0000u);
+        ds_write_b32(base + (2 * e) * VROW, (ev & 0xffffu) | (od << 16));
+        ds_write_b32(base + (2 * e + 1) * VROW, (ev >> 16) | (od & 0xffff0000u));
       }
     }
   };
@@ -1056,18 +1094,22 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   for (int d = 0; d < DT; ++d) O[d] = f32x16_t{};
   float m = -INFINITY, l = 0.f;
 
+  // Every iteration issues the same loads, past the last tile too (keys are
+  // clamped to kmax - 1, so those read valid memory and land in slots nobody
+  // reads): the number of loads in flight is then the same at every point of
+  // the loop, and each wait below is exact rather than a full drain.
   // prologue: K tiles 0 and 1 requested, V^T of tile 0 stored, V of tile 1 in registers
   issue_k(0);
-  if (ntile > 1) issue_k(1);
+  issue_k(1);
   load_v(0);
   store_vt(0);
-  if (ntile > 1) load_v(1);
+  load_v(1);
   for (int t = 0; t < ntile; ++t) {
-    // K tile t landed (loads issued after it: K(t+1) and V(t+1), when they exist)
-    if (t + 1 < ntile) wait_vmcnt<KPW + VPT>(); else wait_vmcnt<0>();
+    // K tile t landed (loads issued after it: K(t+1) and V(t+1))
+    wait_vmcnt<KPW + VPT>();
     barrier();                               // K(t), V^T(t) visible; slots of t-1 free
-    if (t + 2 < ntile) issue_k(t + 2);
-    const unsigned char* sl = sK[t % NKS] + lane * 16;
+    issue_k(t + 2);
+    const unsigned char* sl = (sKd + (t % NKS) * KFR * 1024) + lane * 16;
     // two independent accumulation chains (q hi, q lo) keep the MFMA pipe busy
     f32x16_t S = f32x16_t{}, S2 = f32x16_t{};
 #pragma unroll
@@ -1109,7 +1151,23 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
       for (int d = 0; d < DT; ++d) O[d] *= alpha;
     }
     // O^T += V^T P^T over two 16-key steps; slot j of step u is key 16u + 8(j/4) + 4(l/32) + j%4
-    const unsigned char* vt = sVt[t & 1];
+    // The V^T fragments are read with explicit LDS instructions and an
+    // explicit wait tied to their registers: the compiler, which cannot tell
+    // these reads from the ring slot the direct loads are filling, would
+    // otherwise wait for every load in flight (the K tile two ahead included)
+    // before the first of them. Fragment (u, d): rows 32d + l%32, keys
+    // 16u + 4(l/32) .. +4 and +8 .. +4 (two 8-byte reads 16 bytes apart).
+    const unsigned vrow = lds_addr(sVt0 + (t & 1) * HD * VROW) + c32 * VROW + 8 * hf;
+    u32x4 va[2][DT];
+#pragma unroll
+    for (int d = 0; d < DT; ++d) {
+      va[0][d] = ds_read2_b64<0, 2>(vrow + 32 * d * VROW);
+      va[1][d] = ds_read2_b64<4, 6>(vrow + 32 * d * VROW);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int d = 0; d < DT; ++d) lgkm_wait_for(va[u][d]);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
       unsigned ph[4], pl[4];
@@ -1118,21 +1176,16 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
       const u32x4 pa = u32x4{ph[0], ph[1], ph[2], ph[3]}, pb = u32x4{pl[0], pl[1], pl[2], pl[3]};
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const unsigned char* row = vt + (32 * d + c32) * VROW;
-        const uint2 v0 = *(const uint2*)(row + (16 * u + 4 * hf) * 2);
-        const uint2 v1 = *(const uint2*)(row + (16 * u + 8 + 4 * hf) * 2);
-        const u32x4 va = u32x4{v0.x, v0.y, v1.x, v1.y};
-        O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va), __builtin_bit_cast(bf16x8_t, pa), O[d], 0, 0, 0);
-        O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va), __builtin_bit_cast(bf16x8_t, pb), O[d], 0, 0, 0);
+        O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va[u][d]), __builtin_bit_cast(bf16x8_t, pa), O[d], 0, 0, 0);
+        O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va[u][d]), __builtin_bit_cast(bf16x8_t, pb), O[d], 0, 0, 0);
       }
     }
     // V^T of tile t+1 into the other buffer (its last readers passed this
     // iteration's barrier), then V of tile t+2 into registers
-    if (t + 1 < ntile) {
-      store_vt(t + 1);
-      if (t + 2 < ntile) load_v(t + 2);
-    }
+    store_vt(t + 1);
+    load_v(t + 2);
   }
+  wait_vmcnt<0>();                           // no load may land in LDS after this workgroup ends
   // normalise and store: element e of O[d] is dim 32d + 8(e/4) + 4(l/32) + e%4 of row 32w + l%32
   const int r = 32 * w + c32;
   if (r < it.nq) {
@@ -1424,18 +1477,31 @@ hipError_t launch_attention(hipStream_t st, bool bf16, const AttnItem* items, in
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, int nitems, const float* q,
-                                   const void* kv, const int* bt_store, int layer, int num_blocks, int n_h,
-                                   int n_kv, int hd, float scale, void* out, size_t out_lo) {
+hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, int nitems, int max_keys,
+                                   const float* q, const void* kv, const int* bt_store, int layer, int num_blocks,
+                                   int n_h, int n_kv, int hd, float scale, void* out, size_t out_lo) {
   if (nitems <= 0) return hipSuccess;
+  // K ring (3 stages of hd/16 1 KB fragments), two V^T buffers (hd rows of
+  // 32 keys + 8 pad bytes), the block ids of the longest item
+  const unsigned shm = 3u * (unsigned)(hd / 16) * 1024u + 2u * (unsigned)hd * 72u +
+                       (unsigned)((max_keys + kBlock - 1) / kBlock) * 4u;
+  if (max_keys < 1 || shm > kPrefillLdsMax) return hipErrorInvalidValue;
   const dim3 grid(nitems, n_h), blk(256);
   const float sl2 = scale * 1.4426950408889634f;
+  static bool attr = false;                // one attribute call per process for both instantiations
+  if (!attr) {
+    for (const void* f : {(const void*)k_prefill_attn<64>, (const void*)k_prefill_attn<128>}) {
+      hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kPrefillLdsMax);
+      if (e != hipSuccess) return e;
+    }
+    attr = true;
+  }
   if (hd == 64)
-    klaunch(k_prefill_attn<64>, grid, blk, st, items, q, (const uint16_t*)kv, bt_store, layer, num_blocks, n_h, n_kv,
-            sl2, (uint16_t*)out, out_lo);
+    klaunch_shm(k_prefill_attn<64>, grid, blk, shm, st, items, q, (const uint16_t*)kv, bt_store, layer, num_blocks,
+                n_h, n_kv, sl2, (uint16_t*)out, out_lo);
   else if (hd == 128)
-    klaunch(k_prefill_attn<128>, grid, blk, st, items, q, (const uint16_t*)kv, bt_store, layer, num_blocks, n_h,
-            n_kv, sl2, (uint16_t*)out, out_lo);
+    klaunch_shm(k_prefill_attn<128>, grid, blk, shm, st, items, q, (const uint16_t*)kv, bt_store, layer, num_blocks,
+                n_h, n_kv, sl2, (uint16_t*)out, out_lo);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
