@@ -1134,7 +1134,10 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
 #pragma unroll
     for (int e = 1; e < 16; ++e) mx = fmaxf(mx, S[e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mn = fmaxf(m, mx);
+    // The reference maximum moves only when a score exceeds it by more than
+    // 2^8 (log2 units): probabilities then stay below 256, exact in the split
+    // and harmless in fp32, and the rescale of O below is rare.
+    const float mn = (mx > m + 8.f) ? mx : m;
     const float base = (mn == -INFINITY) ? 0.f : mn;   // a row with no key yet keeps m = -inf
     const float alpha = __builtin_amdgcn_exp2f(m - base);
     float ts = 0.f;
