@@ -1095,6 +1095,9 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
   // output), so the order changes no result.
   std::stable_sort(e->items.begin(), e->items.end(),
                    [](const AttnItem& a, const AttnItem& b) { return a.k1 - a.k0 > b.k1 - b.k0; });
+  // the split combine in the same spirit: rows with the most partial slots first
+  std::stable_sort(e->red.begin(), e->red.end(),
+                   [](const ReduceItem& a, const ReduceItem& b) { return a.nslots > b.nslots; });
   if (!e->plan_only) {
     if (T > e->lay.Tmax || R > e->lay.Rmax || nslots > e->lay.slots_cap ||
         (int64_t)e->items.size() > e->lay.items_cap) {

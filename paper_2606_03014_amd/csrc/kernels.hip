@@ -1203,26 +1203,47 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
 
 // Combine the key-range partials of one row (fixed order over ranges).
 template <bool BF>
-__global__ void k_attn_reduce(const ReduceItem* __restrict__ red, const float* __restrict__ pacc,
-                              const float* __restrict__ pml, void* __restrict__ outv, size_t out_lo, int n_h,
-                              int hd) {
-  const ReduceItem it = red[blockIdx.x];
-  const int h = blockIdx.y;
-  const int dd = threadIdx.x;
+__global__ __launch_bounds__(256) void k_attn_reduce(const ReduceItem* __restrict__ red, const float* __restrict__ pacc,
+                                                     const float* __restrict__ pml, void* __restrict__ outv,
+                                                     size_t out_lo, int n_h, int hd) {
+  // One workgroup per (row, head); G = 256 / hd groups of hd lanes take every
+  // G-th slot, so a row with many key ranges needs G times fewer dependent
+  // load rounds. The slot maximum comes from all 256 lanes at once.
+  __shared__ float sm[4];
+  __shared__ float so[256];
+  __shared__ float sl[4];
+  const ReduceItem it = red[blockIdx.y];
+  const int h = blockIdx.x;
+  const int G = 256 / hd;
+  const int g = threadIdx.x / hd, dd = threadIdx.x % hd;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   float M = -INFINITY;
-#pragma unroll 8
-  for (int s = 0; s < it.nslots; ++s) M = fmaxf(M, pml[((size_t)(it.slot0 + s) * n_h + h) * 2]);
+  for (int s = threadIdx.x; s < it.nslots; s += 256) M = fmaxf(M, pml[((size_t)(it.slot0 + s) * n_h + h) * 2]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
+  if (lane == 0) sm[w] = M;
+  __syncthreads();
+  M = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
   float L = 0.f, o = 0.f;
 #pragma unroll 8
-  for (int s = 0; s < it.nslots; ++s) {
+  for (int s = g; s < it.nslots; s += G) {
     const size_t b = (size_t)(it.slot0 + s) * n_h + h;
-    const float wgt = exp2f(pml[b * 2] - M);
+    const float wgt = __builtin_amdgcn_exp2f(pml[b * 2] - M);
     L += pml[b * 2 + 1] * wgt;
     o += pacc[b * hd + dd] * wgt;
   }
-  const size_t oo = ((size_t)it.row * n_h + h) * hd + dd;
-  if (BF) store_split((uint16_t*)outv, out_lo, oo, o / L);
-  else ((float*)outv)[oo] = o / L;
+  so[threadIdx.x] = o;
+  if (dd == 0) sl[g] = L;
+  __syncthreads();
+  if (g == 0) {
+    for (int k = 1; k < G; ++k) {
+      o += so[k * hd + dd];
+      L += sl[k];
+    }
+    const size_t oo = ((size_t)it.row * n_h + h) * hd + dd;
+    if (BF) store_split((uint16_t*)outv, out_lo, oo, o / L);
+    else ((float*)outv)[oo] = o / L;
+  }
 }
 
 // ------------------------------------------------------------------ argmax
@@ -1514,9 +1535,10 @@ hipError_t launch_attn_reduce(hipStream_t st, bool bf16, const ReduceItem* red, 
                               const float* pacc, const float* pml, void* out, size_t out_lo, int n_h,
                               int hd) {
   if (nred <= 0) return hipSuccess;
-  dim3 grid(nred, n_h);
-  if (bf16) klaunch(k_attn_reduce<true>, dim3(grid), dim3(hd), st, red, pacc, pml, out, out_lo, n_h, hd);
-  else klaunch(k_attn_reduce<false>, dim3(grid), dim3(hd), st, red, pacc, pml, out, out_lo, n_h, hd);
+  if (hd < 64 || hd > 256 || 256 % hd || nred > 65535) return hipErrorInvalidValue;
+  dim3 grid(n_h, nred);                    // heads fastest: a row's heads start together
+  if (bf16) klaunch(k_attn_reduce<true>, grid, dim3(256), st, red, pacc, pml, out, out_lo, n_h, hd);
+  else klaunch(k_attn_reduce<false>, grid, dim3(256), st, red, pacc, pml, out, out_lo, n_h, hd);
   return hipGetLastError();
 }
 
