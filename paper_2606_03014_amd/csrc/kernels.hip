@@ -120,10 +120,12 @@ __device__ __forceinline__ float swz_xor16(float v) {
   return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, v), 0x401F));
 }
 
+// Sum over the 64 lanes (every lane gets it): DPP within rows of 16, a
+// swizzle across the two rows of each half, one exchange across the halves.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v = sum16(v);
+  v += swz_xor16(v);
+  return v + __shfl_xor(v, 32, 64);
 }
 
 // Sum over a 256-thread block; every thread gets the result.
@@ -172,6 +174,19 @@ __global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, con
   const int j = blockIdx.x;
   const int r = gather ? gather[j] : j;
   const int i = threadIdx.x * 4;
+  // the row's gain is fetched first, so its dependent loads (model id, gain
+  // pointer, four gains) overlap the partial-sum loads instead of following
+  // the block reduction
+  const void* g = pick(gamma, row_model[r]);
+  float gv[4];
+  if (BF) {
+    const uint2 gb = *(const uint2*)((const uint16_t*)g + i);
+    gv[0] = __uint_as_float(gb.x << 16); gv[1] = __uint_as_float(gb.x & 0xffff0000u);
+    gv[2] = __uint_as_float(gb.y << 16); gv[3] = __uint_as_float(gb.y & 0xffff0000u);
+  } else {
+    const float4 gf = *(const float4*)((const float*)g + i);
+    gv[0] = gf.x; gv[1] = gf.y; gv[2] = gf.z; gv[3] = gf.w;
+  }
   float4* xr = (float4*)(x + (size_t)r * d + i);
   float4 v = *xr;
   if (nsplit) {
@@ -191,18 +206,17 @@ __global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, con
   float tot = 0.f;
   for (int k = 0; k < nw; ++k) tot += red[k];
   const float scale = rsqrtf(tot / (float)d + eps);
-  const void* g = pick(gamma, row_model[r]);
-  const float y[4] = {v.x * scale, v.y * scale, v.z * scale, v.w * scale};
+  const float y[4] = {v.x * scale * gv[0], v.y * scale * gv[1], v.z * scale * gv[2], v.w * scale * gv[3]};
   if (BF) {
+    // split-bf16 pairs packed in hardware, one 8-byte store per plane
+    unsigned h01, l01, h23, l23;
+    split_pair(y[0], y[1], h01, l01);
+    split_pair(y[2], y[3], h23, l23);
     uint16_t* o = (uint16_t*)out + (size_t)j * d + i;
-    const uint16_t* gg = (const uint16_t*)g + i;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) store_split(o, out_lo, k, y[k] * bf2f(gg[k]));
+    *(uint2*)o = make_uint2(h01, h23);
+    *(uint2*)(o + out_lo) = make_uint2(l01, l23);
   } else {
-    float* o = (float*)out + (size_t)j * d + i;
-    const float* gg = (const float*)g + i;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) o[k] = y[k] * gg[k];
+    *(float4*)((float*)out + (size_t)j * d + i) = make_float4(y[0], y[1], y[2], y[3]);
   }
 }
 
