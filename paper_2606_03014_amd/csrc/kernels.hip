@@ -150,12 +150,21 @@ __global__ __launch_bounds__(256) void k_embed(const int* __restrict__ tok_store
   const int tok = tok_store[row_tok[t]];
   const void* E = pick(embed, row_model[t]);
   float* xr = x + (size_t)t * d;
+  // 16-byte loads, all of a thread's issued before the first store (d % 256 == 0)
   if (BF) {
     const uint16_t* e = (const uint16_t*)E + (size_t)tok * d;
-    for (int i = threadIdx.x; i < d; i += 256) xr[i] = bf2f(e[i]);
+#pragma unroll 2
+    for (int i = threadIdx.x * 8; i < d; i += 256 * 8) {
+      const uint4 u = *(const uint4*)(e + i);
+      *(float4*)(xr + i) = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                                       __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+      *(float4*)(xr + i + 4) = make_float4(__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xffff0000u),
+                                           __uint_as_float(u.w << 16), __uint_as_float(u.w & 0xffff0000u));
+    }
   } else {
     const float* e = (const float*)E + (size_t)tok * d;
-    for (int i = threadIdx.x; i < d; i += 256) xr[i] = e[i];
+#pragma unroll 4
+    for (int i = threadIdx.x * 4; i < d; i += 256 * 4) *(float4*)(xr + i) = *(const float4*)(e + i);
   }
 }
 
@@ -754,13 +763,13 @@ __global__ __launch_bounds__(256) void k_rope_kv(const float* __restrict__ part,
   if (item < npairs) {
     const int head = item / half, jj = item - head * half;
     const int c = head * hd + jj;
+    const float2 cs = tab[(size_t)pos * half + jj];   // in flight with the partial sums
     float x1 = 0.f, x2 = 0.f;
 #pragma unroll 16
     for (int s = 0; s < nsplit; ++s) {
       x1 += pr[(size_t)s * split_stride + c];
       x2 += pr[(size_t)s * split_stride + c + half];
     }
-    const float2 cs = tab[(size_t)pos * half + jj];
     const float y1 = x1 * cs.x - x2 * cs.y;
     const float y2 = x2 * cs.x + x1 * cs.y;
     if (head < n_h) {
@@ -1273,12 +1282,24 @@ __global__ __launch_bounds__(1024) void k_argmax(const float* __restrict__ logit
   int bi = INT_MAX;
   // V % 4 == 0: each thread scans float4 groups in increasing index order, so a
   // strict '>' keeps the lowest index among its equal maxima.
-  for (int v4 = threadIdx.x; v4 < V / 4; v4 += 1024) {
-    const float4 x = *(const float4*)(lr + 4 * v4);
-    if (x.x > best) { best = x.x; bi = 4 * v4; }
-    if (x.y > best) { best = x.y; bi = 4 * v4 + 1; }
-    if (x.z > best) { best = x.z; bi = 4 * v4 + 2; }
-    if (x.w > best) { best = x.w; bi = 4 * v4 + 3; }
+  // Eight groups' loads are issued before any of them is compared.
+  constexpr int B = 8;
+  for (int v0 = threadIdx.x; v0 < V / 4; v0 += 1024 * B) {
+    float4 xs[B];
+#pragma unroll
+    for (int k = 0; k < B; ++k) {
+      const int v4 = v0 + 1024 * k;
+      xs[k] = (v4 < V / 4) ? *(const float4*)(lr + 4 * v4) : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+    }
+#pragma unroll
+    for (int k = 0; k < B; ++k) {
+      const int v4 = v0 + 1024 * k;
+      const float4 x = xs[k];
+      if (x.x > best) { best = x.x; bi = 4 * v4; }
+      if (x.y > best) { best = x.y; bi = 4 * v4 + 1; }
+      if (x.z > best) { best = x.z; bi = 4 * v4 + 2; }
+      if (x.w > best) { best = x.w; bi = 4 * v4 + 3; }
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
