@@ -559,11 +559,19 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) 
       Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
     }
   }
+  // Item order (workgroups of consecutive ids run at the same time on one
+  // XCD): split by split, then supertiles of up to 4 row tiles x 8 column
+  // tiles, rows fastest, so the ~32 workgroups an XCD holds at once share
+  // their activation and weight stages in its L2.
   const int idx = blk - item0;
-  const int mc = idx % n_mc;
-  const int rest = idx / n_mc;
-  const int s = rest % a.S;
-  const int nb = rest / a.S;
+  const int ncol = a.N / BN;
+  const int s = idx / (n_mc * ncol);
+  const int j = idx - s * n_mc * ncol;
+  const int band = j / (4 * ncol), r0 = band * 4, hb = min(4, n_mc - r0);
+  const int j2 = j - band * 4 * ncol;
+  const int chunk = j2 / (hb * 8), j3 = j2 - chunk * hb * 8;
+  const int mc = r0 + j3 % hb;
+  const int nb = chunk * 8 + j3 / hb;
   const int ks0 = s * a.ksteps;
   const int nt0 = nb * (BN / 16);                     // first 16-column weight tile of the block
   const int KS = a.K >> 5;
