@@ -43,6 +43,7 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
@@ -526,6 +527,15 @@ __device__ __forceinline__ u32x4 ds_read2_b64(unsigned addr) {
   u32x4 v;
   asm volatile("ds_read2_b64 %0, %1 offset0:%2 offset1:%3" : "=v"(v) : "v"(addr), "i"(O0), "i"(O1));
   return v;
+}
+// Two transposed 8-byte LDS reads (ds_read_b64_tr_b16) at addr + O0 and
+// addr + O1 into one register quad; untracked like ds_read2_b64 above.
+template <int O0, int O1>
+__device__ __forceinline__ u32x4 ds_read_tr16_pair(unsigned addr) {
+  u32x2_t a, b;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(a) : "v"(addr), "i"(O0));
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(b) : "v"(addr), "i"(O1));
+  return u32x4{a.x, a.y, b.x, b.y};
 }
 // One 4-byte LDS store the compiler does not track (ordered by "memory" and by
 // the explicit LDS waits before each barrier).
@@ -1013,18 +1023,18 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   constexpr int DT = HD / 32;               // 32-dim tiles of O^T
   constexpr int KFR = DS;                   // K fragments (1 KB) per tile
   constexpr int KPW = KFR / 4;              // K fragments loaded per wave
-  constexpr int NKS = 3;                    // K ring stages
-  constexpr int VROW = TK * 2 + 8;          // bytes per V^T row (padded against bank conflicts)
-  constexpr int VCH = TK * HD / 8;          // 16-byte V chunks per tile
-  constexpr int VPT = VCH / 256;            // per thread
-  static_assert(KPW >= 1 && KPW * 4 == KFR && VPT * 256 == VCH, "tile shape");
+  constexpr int ROWB = HD * 2;              // bytes per V row
+  constexpr int CPR = ROWB / 16;            // 16-byte chunks per V row
+  constexpr int KPF = 1024 / ROWB;          // V rows per 1 KB fragment
+  constexpr int VFR = TK * ROWB / 1024;     // V fragments per tile
+  constexpr int VPW = VFR / 4;              // V fragments loaded per wave
+  constexpr int NKS = 3;                    // ring stages (K and V)
+  static_assert(KPW >= 1 && KPW * 4 == KFR && VPW >= 1 && VPW * 4 == VFR, "tile shape");
   // One dynamic LDS block (sized by the launcher): the K ring (NKS x KFR KB),
-  // the two V^T buffers, then the block ids of keys [0, kmax). Keeping all
-  // three in one object lets the explicit waits below order the direct loads
-  // into the ring against the V^T reads.
+  // the V ring (NKS x VFR KB), then the block ids of keys [0, kmax).
   extern __shared__ __align__(1024) unsigned char sKd[];
-  unsigned char* sVt0 = sKd + NKS * KFR * 1024;
-  int* sbt = (int*)(sVt0 + 2 * HD * VROW);
+  unsigned char* sV = sKd + NKS * KFR * 1024;
+  int* sbt = (int*)(sV + NKS * VFR * 1024);
 
   const PrefillItem it = items[blockIdx.x];
   const int h = blockIdx.y;
@@ -1064,57 +1074,46 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   }
   const int qpos = it.pos0 + 32 * w + c32;   // this lane's query position
 
-  // K tile t: fragment s holds key t*32 + l%32, dims 16s + 8(l/32) .. +8 in lane l
-  auto issue_k = [&](int t) {
-    const int key = min(t * TK + c32, kmax - 1);
-    const uint16_t* base = pool + (size_t)sbt[key >> 4] * bstride + (key & 15) * HD + 8 * hf;
-    unsigned char* sl = (sKd + (t % NKS) * KFR * 1024);
+  // Tile t of K and V, both by direct loads into their rings (slot t % NKS).
+  // K fragment s holds key t*32 + l%32, dims 16s + 8(l/32) .. +8 in lane l.
+  // V keeps its natural [key][dim] rows; the 16-byte chunk c of row r sits at
+  // chunk position c ^ 2(r % 4), so the four rows a transposed read touches
+  // fall on different LDS banks.
+  const int vrow_in = lane / CPR, vcp = lane % CPR;
+  auto issue_kv = [&](int t) {
+    {
+      const int key = min(t * TK + c32, kmax - 1);
+      const uint16_t* base = pool + (size_t)sbt[key >> 4] * bstride + (key & 15) * HD + 8 * hf;
+      unsigned char* sl = sKd + (t % NKS) * KFR * 1024;
 #pragma unroll
-    for (int i = 0; i < KPW; ++i) {
-      const int s = w * KPW + i;
-      __builtin_amdgcn_global_load_lds((const void*)(base + 16 * s), MOA_LDS(sl + s * 1024), 16, 0, 0);
-    }
-  };
-  // V chunk c of a tile: key c % 32 (adjacent lanes hold adjacent keys), dims
-  // 8 (c / 32) .. +8
-  u32x4 vr[VPT];
-  auto load_v = [&](int t) {
-#pragma unroll
-    for (int j = 0; j < VPT; ++j) {
-      const int c = threadIdx.x + 256 * j;
-      const int key = min(t * TK + (c & 31), kmax - 1), cc = c >> 5;
-      vr[j] = *(const u32x4*)(pool + (size_t)sbt[key >> 4] * bstride + kBlock * HD + (key & 15) * HD + cc * 8);
-    }
-  };
-  // V^T: row = dim, keys contiguous. The lanes of an even/odd key pair swap
-  // their chunks (one DPP move per word); the even lane then writes dims 0..3
-  // and the odd lane dims 4..7 of the chunk, each as (even key, odd key) words.
-  // The stores are explicit LDS instructions, like the V^T reads: the
-  // compiler would otherwise hold each of them until the direct loads into
-  // the K ring have landed.
-  auto store_vt = [&](int t) {
-    const unsigned vt = lds_addr(sVt0 + (t & 1) * HD * VROW);
-    const bool odd = lane & 1;
-#pragma unroll
-    for (int j = 0; j < VPT; ++j) {
-      const int c = threadIdx.x + 256 * j;
-      const int k2 = (c & 31) & ~1, cc = c >> 5;
-      unsigned pw[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) pw[e] = (unsigned)__builtin_amdgcn_mov_dpp((int)vr[j][e], 0xB1, 0xF, 0xF, true);
-      // the even lane keeps words 0-1 (dims 0..3), the odd lane words 2-3 (dims 4..7)
-      const unsigned mine0 = odd ? vr[j][2] : vr[j][0], mine1 = odd ? vr[j][3] : vr[j][1];
-      const unsigned oth0 = odd ? pw[2] : pw[0], oth1 = odd ? pw[3] : pw[1];
-      const unsigned base = vt + (cc * 8 + (odd ? 4 : 0)) * VROW + k2 * 2;
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const unsigned mine = e ? mine1 : mine0, other = e ? oth1 : oth0;
-        const unsigned ev = odd ? other : mine, od = odd ? mine : other;   // even-key word, odd-key word
-        ds_write_b32(base + (2 * e) * VROW, (ev & 0xffffu) | (od << 16));
-        ds_write_b32(base + (2 * e + 1) * VROW, (ev >> 16) | (od & 0xffff0000u));
+      for (int i = 0; i < KPW; ++i) {
+        const int s = w * KPW + i;
+        __builtin_amdgcn_global_load_lds((const void*)(base + 16 * s), MOA_LDS(sl + s * 1024), 16, 0, 0);
       }
     }
+    unsigned char* vs = sV + (t % NKS) * VFR * 1024;
+#pragma unroll
+    for (int i = 0; i < VPW; ++i) {
+      const int f = w * VPW + i;
+      const int r = f * KPF + vrow_in;                    // row of the tile this lane fills
+      const int key = min(t * TK + r, kmax - 1);
+      const int gc = vcp ^ ((r & 3) << 1);                // chunk of the key's row it brings
+      const uint16_t* src = pool + (size_t)sbt[key >> 4] * bstride + kBlock * HD + (key & 15) * HD + gc * 8;
+      __builtin_amdgcn_global_load_lds((const void*)src, MOA_LDS(vs + f * 1024), 16, 0, 0);
+    }
   };
+  // Transposed V reads (ds_read_b64_tr_b16: within each 16 lanes, lane 4b+e
+  // receives element e of the 8-byte reads of lanes 4a+b, a = 0..3). Lane
+  // 4a+b of group g reads row 16u + 4(l/32) + a (+8), dims
+  // 32d + 16(g%2) + 4b .. +4; after the transpose lane l holds dim 32d + l%32
+  // of rows 16u + 4(l/32) + 0..3 (+8): the A operand of O^T = V^T P^T with the
+  // slot order of P below.
+  const int ta = (lane & 15) >> 2, tb = lane & 3, tg = lane >> 4;
+  unsigned vcol[DT];
+#pragma unroll
+  for (int d = 0; d < DT; ++d)
+    vcol[d] = (unsigned)((((4 * d + 2 * (tg & 1) + (tb >> 1)) ^ (2 * ta)) * 16) + 8 * (tb & 1));
+  const unsigned vrowoff = (unsigned)((4 * hf + ta) * ROWB);
   auto barrier = [] {
     wait_lgkm0();
     asm volatile("s_barrier" ::: "memory");
@@ -1129,17 +1128,13 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
   // clamped to kmax - 1, so those read valid memory and land in slots nobody
   // reads): the number of loads in flight is then the same at every point of
   // the loop, and each wait below is exact rather than a full drain.
-  // prologue: K tiles 0 and 1 requested, V^T of tile 0 stored, V of tile 1 in registers
-  issue_k(0);
-  issue_k(1);
-  load_v(0);
-  store_vt(0);
-  load_v(1);
+  issue_kv(0);
+  issue_kv(1);
   for (int t = 0; t < ntile; ++t) {
-    // K tile t landed (loads issued after it: K(t+1) and V(t+1))
-    wait_vmcnt<KPW + VPT>();
-    barrier();                               // K(t), V^T(t) visible; slots of t-1 free
-    issue_k(t + 2);
+    // tile t landed (loads issued after it: tile t+1's)
+    wait_vmcnt<KPW + VPW>();
+    barrier();                               // tile t visible; slots of t-1 free
+    issue_kv(t + 2);
     const unsigned char* sl = (sKd + (t % NKS) * KFR * 1024) + lane * 16;
     // two independent accumulation chains (q hi, q lo) keep the MFMA pipe busy
     f32x16_t S = f32x16_t{}, S2 = f32x16_t{};
@@ -1185,18 +1180,16 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
       for (int d = 0; d < DT; ++d) O[d] *= alpha;
     }
     // O^T += V^T P^T over two 16-key steps; slot j of step u is key 16u + 8(j/4) + 4(l/32) + j%4
-    // The V^T fragments are read with explicit LDS instructions and an
-    // explicit wait tied to their registers: the compiler, which cannot tell
-    // these reads from the ring slot the direct loads are filling, would
-    // otherwise wait for every load in flight (the K tile two ahead included)
-    // before the first of them. Fragment (u, d): rows 32d + l%32, keys
-    // 16u + 4(l/32) .. +4 and +8 .. +4 (two 8-byte reads 16 bytes apart).
-    const unsigned vrow = lds_addr(sVt0 + (t & 1) * HD * VROW) + c32 * VROW + 8 * hf;
+    // The V reads are explicit LDS instructions with an explicit wait tied to
+    // their registers: the compiler, which cannot tell them from the ring
+    // slots the direct loads are filling, would otherwise wait for every load
+    // in flight (the tile two ahead included) before the first of them.
+    const unsigned vb = lds_addr(sV + (t % NKS) * VFR * 1024) + vrowoff;
     u32x4 va[2][DT];
 #pragma unroll
     for (int d = 0; d < DT; ++d) {
-      va[0][d] = ds_read2_b64<0, 2>(vrow + 32 * d * VROW);
-      va[1][d] = ds_read2_b64<4, 6>(vrow + 32 * d * VROW);
+      va[0][d] = ds_read_tr16_pair<0 * ROWB, 8 * ROWB>(vb + vcol[d]);
+      va[1][d] = ds_read_tr16_pair<16 * ROWB, 24 * ROWB>(vb + vcol[d]);
     }
 #pragma unroll
     for (int u = 0; u < 2; ++u)
@@ -1214,10 +1207,6 @@ __global__ __launch_bounds__(256, PREFILL_WPE) void k_prefill_attn(const Prefill
         O[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, va[u][d]), __builtin_bit_cast(bf16x8_t, pb), O[d], 0, 0, 0);
       }
     }
-    // V^T of tile t+1 into the other buffer (its last readers passed this
-    // iteration's barrier), then V of tile t+2 into registers
-    store_vt(t + 1);
-    load_v(t + 2);
   }
   wait_vmcnt<0>();                           // no load may land in LDS after this workgroup ends
   // normalise and store: element e of O[d] is dim 32d + 8(e/4) + 4(l/32) + e%4 of row 32w + l%32
@@ -1548,9 +1537,9 @@ hipError_t launch_prefill_attention(hipStream_t st, const PrefillItem* items, in
                                    const float* q, const void* kv, const int* bt_store, int layer, int num_blocks,
                                    int n_h, int n_kv, int hd, float scale, void* out, size_t out_lo) {
   if (nitems <= 0) return hipSuccess;
-  // K ring (3 stages of hd/16 1 KB fragments), two V^T buffers (hd rows of
-  // 32 keys + 8 pad bytes), the block ids of the longest item
-  const unsigned shm = 3u * (unsigned)(hd / 16) * 1024u + 2u * (unsigned)hd * 72u +
+  // K ring (3 stages of hd/16 1 KB fragments), V ring (3 tiles of 32 rows of
+  // hd values), the block ids of the longest item
+  const unsigned shm = 3u * (unsigned)(hd / 16) * 1024u + 3u * 32u * (unsigned)hd * 2u +
                        (unsigned)((max_keys + kBlock - 1) / kBlock) * 4u;
   if (max_keys < 1 || shm > kPrefillLdsMax) return hipErrorInvalidValue;
   const dim3 grid(nitems, n_h), blk(256);
