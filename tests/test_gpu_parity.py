@@ -207,6 +207,22 @@ def test_bf16_8b_width_long_prompt_chunked_prefill():
         say(f"8b-wide long req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
 
 
+def test_bf16_1b_width_long_prompt_prefill():
+    """Real 1B width (head_dim 64), two layers: a 6,000-token prompt prefilled
+    in chunks of 4,096 (the causal kernel stages 375 block ids in LDS and runs
+    ~190 key tiles per query block) beside a short decoding request;
+    teacher-forced against the oracle."""
+    shape = replace(LLAMA_1B, n_layers=2)
+    consts = EngineConsts(num_kv_blocks=1024, max_num_seqs=8, max_prefill_tokens=4096, max_model_len=8192)
+    ws = [generate_weights(LLAMA_1B, "bf16", 3, 2, 0, n_layers=2)]
+    prompts = _prompts(shape.vocab, [6000, 90], 8)
+    reqs = [(prompts[0], 0, 3), (prompts[1], 0, 40)]
+    toks, logs = run_requests(shape, "bf16", consts, ws, reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, flips = compare(shape, ws[m], p, t, lg, True, 2e-2, what=f"long 1b req{i}")
+        say(f"1b-wide long req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+
+
 def test_bf16_injected_history_pareto_lengths():
     """Calls that arrive with a bf16 K/V history (straggler workload): real
     8B width, two layers, histories at quantiles of the Pareto(1.2) length law
