@@ -369,7 +369,12 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     return;
   }
   const int KS = K / 32;
-  if (maxM >= kBigMinRows && N % 256 == 0) {
+  // Below 256 rows the 128-row tile still wins where its per-workgroup set-up
+  // is amortised over a long k run: square and deep-K projections (N <= K)
+  // from 160 rows, wide ones with K >= 4096 from 192 (cold-weight sweeps of
+  // both model widths, one and four groups)
+  const int big_min = N <= K ? 160 : (K >= 4096 ? 192 : kBigMinRows);
+  if (maxM >= big_min && N % 256 == 0) {
     // matrix-core bound: 128-row tiles on the 32x32 MFMA, split-K only to
     // give every CU a workgroup
     mt = kBigTile;

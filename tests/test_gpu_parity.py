@@ -274,13 +274,15 @@ def test_bf16_injected_history_pareto_lengths():
         assert err <= 2e-2
 
 
-@pytest.mark.parametrize("n", [100, 300], ids=["100-rows", "300-rows"])
+@pytest.mark.parametrize("n", [100, 180, 300], ids=["100-rows", "180-rows", "300-rows"])
 def test_bf16_wide_decode_batch(n):
     """A decode batch of n rows of one 8B-width model (two layers): every
     projection and the LM head run as one n-row group. 300 rows take the
     large-M 32x32-MFMA GEMM (the shape of the straggler workload's refill
     phase), 100 rows the workgroup-tile kernel with its widest tiles (64 rows
-    x 256 columns). Eight of the calls carry a host K/V history and are
+    x 256 columns), 180 rows both: the square and deep-K projections (o,
+    down) on 128-row tiles with a partly empty second tile, the wide ones
+    (qkv, gate-up, LM head) on workgroup tiles. Eight of the calls carry a host K/V history and are
     checked teacher-forced against the oracle; the rest have device-filled
     histories and only set the batch shape."""
     from moa_inputs import f32_to_bf16_bits
