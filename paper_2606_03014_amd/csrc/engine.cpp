@@ -372,9 +372,15 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
   // Below 256 rows the 128-row tile still wins where its per-workgroup set-up
   // is amortised over a long k run: square and deep-K projections (N <= K)
   // from 160 rows, wide ones with K >= 4096 from 192 (cold-weight sweeps of
-  // both model widths, one and four groups)
+  // both model widths, one and four equal groups). Only when every non-empty
+  // group has that many rows: small groups beside one large one would pad
+  // their rows to 128 (one large and three small experts ran 54 us per launch
+  // on 128-row tiles against 42 us on workgroup tiles).
   const int big_min = N <= K ? 160 : (K >= 4096 ? 192 : kBigMinRows);
-  if (maxM >= big_min && N % 256 == 0) {
+  int minM = maxM;
+  for (int g = 0; g < in.ngroups; ++g)
+    if (in.nrows[g] > 0) minM = std::min(minM, in.nrows[g]);
+  if ((maxM >= kBigMinRows || minM >= big_min) && N % 256 == 0) {
     // matrix-core bound: 128-row tiles on the 32x32 MFMA, split-K only to
     // give every CU a workgroup
     mt = kBigTile;
