@@ -25,6 +25,11 @@ constexpr int kStageSlots = 4;    // steps that may be in flight (pinned staging
 constexpr int kTargetWaves = 4096;
 constexpr int kBigMinRows = 256;    // a row group this large goes to the 32x32-MFMA GEMM
 constexpr int kBigTargetWgs = 256;  // one workgroup per CU
+// bf16 steps with several models run them on this many streams (the step's
+// model groups split in two halves, the second half on a stream forked from
+// the caller's and joined at the end of the step), so one half's
+// launch-bound kernels and grid tails overlap the other half's work
+constexpr int kModelStreams = 2;
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -98,7 +103,7 @@ struct Layout {
   size_t esz;
   int64_t Tmax, Rmax, slots_cap, items_cap, red_cap, part_cap;
   size_t model_bytes, kv_bytes, block_bytes;
-  size_t off_kv, off_tok, off_bt, off_rope, off_meta, off_x, off_xn, off_part, off_q, off_ao, off_h,
+  size_t off_kv, off_tok, off_bt, off_rope, off_meta, off_x, off_xn, off_part, off_part2, off_q, off_ao, off_h,
       off_logits, off_pacc, off_pml, off_models, total;
   int64_t token_store, block_store, meta_ints;
 };
@@ -160,6 +165,9 @@ Layout make_layout(const moa_engine_cfg& c) {
   // GEMM inputs (xn, ao, h) hold two planes: bf16 hi and lo (fp32 mode uses the first)
   L.off_xn = take((size_t)2 * L.Tmax * d * L.esz);
   L.off_part = take((size_t)L.part_cap * 4);
+  // the second model stream's split-K partials (its projections run while
+  // the first stream's, of another width, are in flight)
+  L.off_part2 = (c.dtype == MOA_BF16 && kModelStreams > 1 && c.max_models > 1) ? take((size_t)L.part_cap * 4) : 0;
   L.off_q = take((size_t)L.Tmax * nh * hd * 4);
   L.off_ao = take((size_t)2 * L.Tmax * nh * hd * L.esz);
   L.off_h = take((size_t)2 * L.Tmax * F * L.esz);
@@ -181,6 +189,8 @@ struct moa_engine {
   bool broken = false;
   hipStream_t stream = nullptr;
   hipStream_t copy_stream = nullptr;
+  hipStream_t stream2 = nullptr;      // second model stream (bf16, several models)
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
   char* arena = nullptr;
   size_t arena_bytes = 0;
   size_t model_top = 0;
@@ -205,6 +215,7 @@ struct moa_engine {
   float* x = nullptr;
   void* xn = nullptr;
   float* part = nullptr;
+  float* part2 = nullptr;             // second model stream's partials
   float* q = nullptr;
   void* ao = nullptr;
   void* h = nullptr;
@@ -235,6 +246,10 @@ struct moa_engine {
   std::vector<AttnItem> items;
   std::vector<ReduceItem> red;
   std::vector<PrefillItem> pitems;
+  // the second stream's share of the step: its first model group, row and
+  // LM row, and where its items start (each list holds the first stream's
+  // items first); split_group == number of groups: one stream
+  int split_group = 0, split_row = 0, split_lm = 0, split_item = 0, split_red = 0, split_pre = 0;
 };
 
 namespace {
@@ -343,10 +358,15 @@ struct GemmPlanIn {
 
 // Choose the tiling and k-split of one grouped GEMM and fill its arguments.
 // X is a split-bf16 pair (lo plane x_lo elements after hi) in bf16 mode.
-void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi, const void* X, size_t x_lo,
-               float* out, uint16_t* hout, size_t h_lo, bool allow_split, GemmArgs& a, int& mt, int& nt) {
+// Tile, split and partial stride are chosen from every group of `in` (the
+// whole step, so a launch that carries only the groups [g0, g0 + ng) plans
+// the same way and writes its partials where the consumer of the whole step
+// expects them); the arguments carry only those groups.
+void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K, int N, int epi, const void* X,
+               size_t x_lo, float* out, uint16_t* hout, size_t h_lo, bool allow_split, GemmArgs& a, int& mt,
+               int& nt) {
   std::memset(&a, 0, sizeof(a));
-  a.ngroups = in.ngroups;
+  a.ngroups = ng;
   a.X = X;
   a.x_lo = x_lo;
   a.h_lo = h_lo;
@@ -359,11 +379,12 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
   if (!e->bf16) {
     mt = 1; nt = 1;
     int item = 0;
-    for (int g = 0; g < in.ngroups; ++g) {
-      a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
-      a.g[g].n_mc = (in.nrows[g] + 15) / 16;
-      a.g[g].item0 = item;
-      item += a.g[g].n_mc * (N / 64);
+    for (int k = 0; k < ng; ++k) {
+      const int g = g0 + k;
+      a.g[k].W = in.W[g]; a.g[k].row0 = in.row0[g]; a.g[k].nrows = in.nrows[g];
+      a.g[k].n_mc = (in.nrows[g] + 15) / 16;
+      a.g[k].item0 = item;
+      item += a.g[k].n_mc * (N / 64);
     }
     a.S = 1; a.ksteps = 0; a.out_split = 0; a.total_items = item;
     return;
@@ -397,11 +418,12 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
     a.ksteps = KS / S;
     a.out_split = (size_t)totalM * N;
     int item = 0;
-    for (int g = 0; g < in.ngroups; ++g) {
-      a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
-      a.g[g].n_mc = (in.nrows[g] + 127) / 128;
-      a.g[g].item0 = item;
-      item += a.g[g].n_mc * S * tiles;
+    for (int k = 0; k < ng; ++k) {
+      const int g = g0 + k;
+      a.g[k].W = in.W[g]; a.g[k].row0 = in.row0[g]; a.g[k].nrows = in.nrows[g];
+      a.g[k].n_mc = (in.nrows[g] + 127) / 128;
+      a.g[k].item0 = item;
+      item += a.g[k].n_mc * S * tiles;
     }
     a.total_items = item;
     return;
@@ -441,11 +463,12 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int K, int N, int epi,
   a.ksteps = KS / S;
   a.out_split = (size_t)totalM * N;  // partial s lives at out + s * rows * N
   int item = 0;
-  for (int g = 0; g < in.ngroups; ++g) {
-    a.g[g].W = in.W[g]; a.g[g].row0 = in.row0[g]; a.g[g].nrows = in.nrows[g];
-    a.g[g].n_mc = (in.nrows[g] + rows_per - 1) / rows_per;
-    a.g[g].item0 = item;
-    item += a.g[g].n_mc * S * tiles;
+  for (int k = 0; k < ng; ++k) {
+    const int g = g0 + k;
+    a.g[k].W = in.W[g]; a.g[k].row0 = in.row0[g]; a.g[k].nrows = in.nrows[g];
+    a.g[k].n_mc = (in.nrows[g] + rows_per - 1) / rows_per;
+    a.g[k].item0 = item;
+    item += a.g[k].n_mc * S * tiles;
   }
   a.total_items = item;
 }
@@ -506,6 +529,7 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
     e->x = (float*)(A + L.off_x);
     e->xn = A + L.off_xn;
     e->part = (float*)(A + L.off_part);
+    e->part2 = L.off_part2 ? (float*)(A + L.off_part2) : nullptr;
     e->q = (float*)(A + L.off_q);
     e->ao = A + L.off_ao;
     e->h = A + L.off_h;
@@ -514,6 +538,11 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
     e->pml = (float*)(A + L.off_pml);
     hipError_t err = hipStreamCreateWithFlags(&e->copy_stream, hipStreamNonBlocking);
     for (int i = 0; i < kStageSlots && err == hipSuccess; ++i) err = hipEventCreateWithFlags(&e->ev[i], hipEventDisableTiming);
+    if (err == hipSuccess && e->part2) {
+      err = hipStreamCreateWithFlags(&e->stream2, hipStreamNonBlocking);
+      if (err == hipSuccess) err = hipEventCreateWithFlags(&e->ev_fork, hipEventDisableTiming);
+      if (err == hipSuccess) err = hipEventCreateWithFlags(&e->ev_join, hipEventDisableTiming);
+    }
     if (err == hipSuccess) {
       // RoPE table: angle pos * theta^(-2i/hd) and its cos/sin in double, stored as fp32.
       const int hd = cfg->model.head_dim, half = hd / 2;
@@ -540,6 +569,7 @@ void moa_destroy(moa_engine* e) {
   if (!e) return;
   if (!e->plan_only) {
     if (e->stream) (void)hipStreamSynchronize(e->stream);
+    if (e->stream2) (void)hipStreamSynchronize(e->stream2);
     for (int i = 0; i < kStageSlots; ++i) {
       if (e->stage[i].buf) (void)hipHostFree(e->stage[i].buf);
       if (e->ev[i]) (void)hipEventDestroy(e->ev[i]);
@@ -548,6 +578,9 @@ void moa_destroy(moa_engine* e) {
     for (auto& t : e->timed) { (void)hipEventDestroy(t.a); (void)hipEventDestroy(t.b); }
     for (hipEvent_t v : e->ev_pool) (void)hipEventDestroy(v);
     if (e->copy_stream) (void)hipStreamDestroy(e->copy_stream);
+    if (e->stream2) (void)hipStreamDestroy(e->stream2);
+    if (e->ev_fork) (void)hipEventDestroy(e->ev_fork);
+    if (e->ev_join) (void)hipEventDestroy(e->ev_join);
   }
   delete e;
 }
@@ -878,92 +911,165 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
     bytes = a.ngroups * (double)a.N * a.K * esz + rows * a.K * 4.0 + out_elems * 4.0;
     flops = 2.0 * rows * a.N * a.K;
   };
-  double kv_keys = 0;
-  int max_item_blocks = 1;
-  for (const AttnItem& it : e->items) {
-    kv_keys += it.k1 - it.k0;
-    max_item_blocks = std::max(max_item_blocks, ((it.k1 - 1) >> 4) - (it.k0 >> 4) + 1);
+
+  // Each stream's share of the layers: rows [r0, r0 + nr), model groups
+  // [g0, g0 + ng) and its slices of the item lists. Every buffer the layers
+  // touch is indexed by row (or by the row's partial slots and KV blocks),
+  // except the split-K partials, which take one buffer per stream.
+  struct Share {
+    hipStream_t st;
+    float* part;
+    int r0, nr, g0, ng;
+    const AttnItem* items;
+    const ReduceItem* red;
+    const PrefillItem* pre;
+    int nitems, nred, npre, max_item_blocks, pre_max_keys;
+    double attn_bytes, attn_flops, pre_bytes, pre_flops, red_bytes;
+    int prev_split;
+    size_t prev_stride;
+  };
+  const int nshare = e->split_group < gin.ngroups ? 2 : 1;
+  Share sh[2];
+  for (int u = 0; u < nshare; ++u) {
+    Share& b = sh[u];
+    const bool first = u == 0;
+    b.st = first ? e->stream : e->stream2;
+    b.part = first ? e->part : e->part2;
+    b.r0 = first ? 0 : e->split_row;
+    b.nr = first ? e->split_row : T - e->split_row;
+    b.g0 = first ? 0 : e->split_group;
+    b.ng = first ? e->split_group : gin.ngroups - e->split_group;
+    const int i0 = first ? 0 : e->split_item, d0 = first ? 0 : e->split_red, p0 = first ? 0 : e->split_pre;
+    b.nitems = first ? e->split_item : nitems - e->split_item;
+    b.nred = first ? e->split_red : nred - e->split_red;
+    b.npre = first ? e->split_pre : npre - e->split_pre;
+    b.items = sd.items + i0;
+    b.red = sd.red + d0;
+    b.pre = sd.pre + p0;
+    double kv_keys = 0;
+    b.max_item_blocks = 1;
+    for (int i = i0; i < i0 + b.nitems; ++i) {
+      const AttnItem& it = e->items[i];
+      kv_keys += it.k1 - it.k0;
+      b.max_item_blocks = std::max(b.max_item_blocks, ((it.k1 - 1) >> 4) - (it.k0 >> 4) + 1);
+    }
+    // causal prefill blocks: K/V of keys [0, pos0 + nq) once per KV head; q.k and p.v per (row, key <= pos)
+    double pre_keys = 0, pre_pairs = 0, pre_rows = 0;
+    b.pre_max_keys = 1;
+    for (int i = p0; i < p0 + b.npre; ++i) {
+      const PrefillItem& pi = e->pitems[i];
+      pre_keys += pi.pos0 + pi.nq;
+      b.pre_max_keys = std::max(b.pre_max_keys, pi.pos0 + pi.nq);
+      pre_pairs += (double)pi.nq * pi.pos0 + (double)pi.nq * (pi.nq + 1) / 2;
+      pre_rows += pi.nq;
+    }
+    double nsl = 0;
+    for (int i = d0; i < d0 + b.nred; ++i) nsl += e->red[i].nslots;
+    b.pre_bytes = pre_keys * nkv * 2.0 * hd * esz + pre_rows * nh * hd * 8.0;
+    b.pre_flops = pre_pairs * nh * hd * 4.0;
+    b.attn_bytes = kv_keys * nkv * 2.0 * hd * esz + (double)b.nr * nh * hd * 8.0;
+    b.attn_flops = kv_keys * nh * hd * 4.0;
+    b.red_bytes = nsl * nh * (hd + 2) * 4.0;
+    b.prev_split = 0;
+    b.prev_stride = 0;
   }
-  // causal prefill blocks: K/V of keys [0, pos0 + nq) once per KV head; q.k and p.v per (row, key <= pos)
-  double pre_keys = 0, pre_pairs = 0, pre_rows = 0;
-  int pre_max_keys = 1;
-  for (const PrefillItem& pi : e->pitems) {
-    pre_keys += pi.pos0 + pi.nq;
-    pre_max_keys = std::max(pre_max_keys, pi.pos0 + pi.nq);
-    pre_pairs += (double)pi.nq * pi.pos0 + (double)pi.nq * (pi.nq + 1) / 2;
-    pre_rows += pi.nq;
-  }
-  const double pre_bytes = pre_keys * nkv * 2.0 * hd * esz + pre_rows * nh * hd * 8.0;
-  const double pre_flops = pre_pairs * nh * hd * 4.0;
-  const double attn_bytes = kv_keys * nkv * 2.0 * hd * esz + (double)T * nh * hd * 8.0;
-  const double attn_flops = kv_keys * nh * hd * 4.0;
-  const double norm_bytes = (double)T * d * 12.0;
   double gb = 0, gf = 0;
 
   if (T > 0) {
-    LAUNCH(MOA_K_EMBED, (double)T * d * (4.0 + esz), 0,
-           launch_embed(s, bf, e->tok_store, sd.row_tok, sd.row_model,
-                        fill([](const ModelDev& x) { return x.embed; }), e->x, T, d), "embed");
-    int prev_split = 0;
-    size_t prev_stride = 0;
+    if (nshare > 1) {
+      HIPCHK(hipEventRecord(e->ev_fork, s), "stream fork");
+      HIPCHK(hipStreamWaitEvent(e->stream2, e->ev_fork, 0), "stream fork");
+    }
+    for (int u = 0; u < nshare; ++u) {
+      const Share& b = sh[u];
+      LAUNCH(MOA_K_EMBED, (double)b.nr * d * (4.0 + esz), 0,
+             launch_embed(b.st, bf, e->tok_store, sd.row_tok + b.r0, sd.row_model + b.r0,
+                          fill([](const ModelDev& x) { return x.embed; }), e->x + (size_t)b.r0 * d, b.nr, d),
+             "embed");
+    }
     for (int l = 0; l < g.n_layers; ++l) {
-      GemmArgs ga;
-      int mt, nt;
-      LAUNCH(MOA_K_NORM, norm_bytes + prev_split * (double)T * d * 4.0, 0,
-             launch_add_rmsnorm(s, bf, e->x, prev_split ? e->part : nullptr, prev_split, prev_stride, nullptr,
-                                sd.row_model, T, fill([l](const ModelDev& x) { return x.attn_norm[l]; }), e->xn,
-                                xn_lo, d, g.rms_eps), "attn norm");
-      plan_gemm(e, weights([l](const ModelDev& x) { return x.wqkv[l]; }), d, qkv, EPI_F32, e->xn, xn_lo, e->part,
-                nullptr, 0, true, ga, mt, nt);
-      gemm_cost(ga, EPI_F32, gb, gf);
-      LAUNCH(MOA_K_GEMM_QKV, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "qkv gemm");
-      LAUNCH(MOA_K_ROPE_KV, (double)T * qkv * 4.0 * ga.S + (double)T * (nh * hd * 4.0 + 2.0 * nkv * hd * esz), 0,
-             launch_rope_kv(s, bf, e->part, ga.S, ga.out_split, sd.row_pos, sd.row_bt, e->bt_store, e->rope, e->q,
-                            e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd, T), "rope kv");
-      if (npre > 0)
-        LAUNCH(MOA_K_PREFILL_ATTN, pre_bytes, pre_flops,
-               launch_prefill_attention(s, sd.pre, npre, pre_max_keys, e->q, e->kv, e->bt_store, l, e->cfg.num_kv_blocks, nh, nkv,
-                                        hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo), "prefill attention");
-      if (nitems > 0)
-        LAUNCH(MOA_K_ATTN, attn_bytes, attn_flops,
-               launch_attention(s, bf, sd.items, nitems, max_item_blocks, e->q, e->kv, e->bt_store, sd.row_bt, l,
-                                e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo, e->pacc,
-                                e->pml), "attention");
-      if (nred > 0)
-        LAUNCH(MOA_K_ATTN_REDUCE, (double)nslots_total(e) * nh * (hd + 2) * 4.0, 0,
-               launch_attn_reduce(s, bf, sd.red, nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
-      plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), nh * hd, d, EPI_F32, e->ao, ao_lo, e->part,
-                nullptr, 0, true, ga, mt, nt);
-      gemm_cost(ga, EPI_F32, gb, gf);
-      LAUNCH(MOA_K_GEMM_O, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "o gemm");
-      LAUNCH(MOA_K_NORM, norm_bytes + ga.S * (double)T * d * 4.0, 0,
-             launch_add_rmsnorm(s, bf, e->x, e->part, ga.S, ga.out_split, nullptr, sd.row_model, T,
-                                fill([l](const ModelDev& x) { return x.mlp_norm[l]; }), e->xn, xn_lo, d,
-                                g.rms_eps), "mlp norm");
-      if (bf) {
-        plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), d, 2 * F, EPI_SWIGLU, e->xn, xn_lo,
-                  nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt);
-        gemm_cost(ga, EPI_SWIGLU, gb, gf);
-        LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(s, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
-      } else {
-        plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), d, 2 * F, EPI_F32, e->xn, 0, e->part,
-                  nullptr, 0, false, ga, mt, nt);
+      for (int u = 0; u < nshare; ++u) {
+        Share& b = sh[u];
+        hipStream_t st = b.st;
+        const size_t ro = (size_t)b.r0;
+        void* xn_b = (char*)e->xn + ro * d * L.esz;
+        const double norm_bytes = (double)b.nr * d * 12.0;
+        GemmArgs ga;
+        int mt, nt;
+        LAUNCH(MOA_K_NORM, norm_bytes + b.prev_split * (double)b.nr * d * 4.0, 0,
+               launch_add_rmsnorm(st, bf, e->x + ro * d, b.prev_split ? b.part + ro * d : nullptr, b.prev_split,
+                                  b.prev_stride, nullptr, sd.row_model + ro, b.nr,
+                                  fill([l](const ModelDev& x) { return x.attn_norm[l]; }), xn_b, xn_lo, d,
+                                  g.rms_eps), "attn norm");
+        plan_gemm(e, weights([l](const ModelDev& x) { return x.wqkv[l]; }), b.g0, b.ng, d, qkv, EPI_F32, e->xn,
+                  xn_lo, b.part, nullptr, 0, true, ga, mt, nt);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
-        HIPCHK(launch_swiglu_f32(s, e->part, (float*)e->h, T, F), "swiglu");
+        LAUNCH(MOA_K_GEMM_QKV, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "qkv gemm");
+        LAUNCH(MOA_K_ROPE_KV, (double)b.nr * qkv * 4.0 * ga.S + (double)b.nr * (nh * hd * 4.0 + 2.0 * nkv * hd * esz), 0,
+               launch_rope_kv(st, bf, b.part + ro * qkv, ga.S, ga.out_split, sd.row_pos + ro, sd.row_bt + ro,
+                              e->bt_store, e->rope, e->q + ro * nh * hd, e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd,
+                              b.nr), "rope kv");
+        if (b.npre > 0)
+          LAUNCH(MOA_K_PREFILL_ATTN, b.pre_bytes, b.pre_flops,
+                 launch_prefill_attention(st, b.pre, b.npre, b.pre_max_keys, e->q, e->kv, e->bt_store, l,
+                                          e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao,
+                                          ao_lo), "prefill attention");
+        if (b.nitems > 0)
+          LAUNCH(MOA_K_ATTN, b.attn_bytes, b.attn_flops,
+                 launch_attention(st, bf, b.items, b.nitems, b.max_item_blocks, e->q, e->kv, e->bt_store, sd.row_bt,
+                                  l, e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo,
+                                  e->pacc, e->pml), "attention");
+        if (b.nred > 0)
+          LAUNCH(MOA_K_ATTN_REDUCE, b.red_bytes, 0,
+                 launch_attn_reduce(st, bf, b.red, b.nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
+        plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), b.g0, b.ng, nh * hd, d, EPI_F32, e->ao,
+                  ao_lo, b.part, nullptr, 0, true, ga, mt, nt);
+        gemm_cost(ga, EPI_F32, gb, gf);
+        LAUNCH(MOA_K_GEMM_O, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "o gemm");
+        LAUNCH(MOA_K_NORM, norm_bytes + ga.S * (double)b.nr * d * 4.0, 0,
+               launch_add_rmsnorm(st, bf, e->x + ro * d, b.part + ro * d, ga.S, ga.out_split, nullptr,
+                                  sd.row_model + ro, b.nr, fill([l](const ModelDev& x) { return x.mlp_norm[l]; }),
+                                  xn_b, xn_lo, d, g.rms_eps), "mlp norm");
+        if (bf) {
+          plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), b.g0, b.ng, d, 2 * F, EPI_SWIGLU,
+                    e->xn, xn_lo, nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt);
+          gemm_cost(ga, EPI_SWIGLU, gb, gf);
+          LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(st, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
+        } else {
+          plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), b.g0, b.ng, d, 2 * F, EPI_F32, e->xn, 0,
+                    b.part, nullptr, 0, false, ga, mt, nt);
+          gemm_cost(ga, EPI_F32, gb, gf);
+          LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
+          HIPCHK(launch_swiglu_f32(st, b.part + ro * 2 * F, (float*)e->h + ro * F, b.nr, F), "swiglu");
+        }
+        plan_gemm(e, weights([l](const ModelDev& x) { return x.wdown[l]; }), b.g0, b.ng, F, d, EPI_F32, e->h, h_lo,
+                  b.part, nullptr, 0, true, ga, mt, nt);
+        gemm_cost(ga, EPI_F32, gb, gf);
+        LAUNCH(MOA_K_GEMM_DOWN, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "down gemm");
+        b.prev_split = ga.S;
+        b.prev_stride = ga.out_split;
       }
-      plan_gemm(e, weights([l](const ModelDev& x) { return x.wdown[l]; }), F, d, EPI_F32, e->h, h_lo, e->part,
-                nullptr, 0, true, ga, mt, nt);
-      gemm_cost(ga, EPI_F32, gb, gf);
-      LAUNCH(MOA_K_GEMM_DOWN, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "down gemm");
-      prev_split = ga.S;
-      prev_stride = ga.out_split;
+    }
+    // The final norm, LM head and argmax run on the caller's stream once both
+    // shares are done: their rows are numbered in LM order, which overlaps
+    // the other share's rows in xn and in the partials.
+    if (nshare > 1) {
+      HIPCHK(hipEventRecord(e->ev_join, e->stream2), "stream join");
+      HIPCHK(hipStreamWaitEvent(s, e->ev_join, 0), "stream join");
     }
     if (R > 0) {
-      LAUNCH(MOA_K_NORM, (double)R * d * (12.0 + prev_split * 4.0), 0,
-             launch_add_rmsnorm(s, bf, e->x, e->part, prev_split, prev_stride, sd.lm_src, sd.row_model, R,
-                                fill([](const ModelDev& x) { return x.final_norm; }), e->xn, xn_lo, d,
-                                g.rms_eps), "final norm");
+      // every share's last down projection was planned over the whole step:
+      // same split and stride; the gather reads each row from its share's partials
+      const int prev_split = sh[0].prev_split;
+      const size_t prev_stride = sh[0].prev_stride;
+      for (int u = 0; u < nshare; ++u) {
+        const int b0 = u == 0 ? 0 : e->split_lm, nb = u == 0 ? e->split_lm : R - e->split_lm;
+        if (nb == 0) continue;
+        LAUNCH(MOA_K_NORM, (double)nb * d * (12.0 + prev_split * 4.0), 0,
+               launch_add_rmsnorm(s, bf, e->x, sh[u].part, prev_split, prev_stride, sd.lm_src + b0, sd.row_model, nb,
+                                  fill([](const ModelDev& x) { return x.final_norm; }),
+                                  (char*)e->xn + (size_t)b0 * d * L.esz, xn_lo, d, g.rms_eps), "final norm");
+      }
       GemmPlanIn lin;
       int lr0 = 0;
       for (int m = 0; m < M; ++m) {
@@ -976,7 +1082,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
       }
       GemmArgs ga;
       int mt, nt;
-      plan_gemm(e, lin, d, V, EPI_F32, e->xn, xn_lo, e->logits, nullptr, 0, false, ga, mt, nt);
+      plan_gemm(e, lin, 0, lin.ngroups, d, V, EPI_F32, e->xn, xn_lo, e->logits, nullptr, 0, false, ga, mt, nt);
       gemm_cost(ga, EPI_F32, gb, gf);
       LAUNCH(MOA_K_GEMM_LMHEAD, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "lm head");
       LAUNCH(MOA_K_ARGMAX, (double)R * V * 4.0, 0, launch_argmax(s, e->logits, R, V, sd.lm_dst, e->tok_store),
@@ -1100,15 +1206,47 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
     }
   }
   const int R = (int)e->l_src.size();
-  // Launch order of the decode-attention items: full-length key ranges first,
-  // then the shorter ones by decreasing length, so the grid ends on its
-  // shortest workgroups. Every item writes its own partial slot (or its row's
-  // output), so the order changes no result.
-  std::stable_sort(e->items.begin(), e->items.end(),
-                   [](const AttnItem& a, const AttnItem& b) { return a.k1 - a.k0 > b.k1 - b.k0; });
+  // Streams: the first half of the step's model groups (rows [0, split_row))
+  // on the caller's stream, the rest on the second stream.
+  int ngrp = 0;
+  for (int m = 0; m < M; ++m) ngrp += grp_rows[m] > 0;
+  e->split_group = ngrp;
+  e->split_row = T;
+  e->split_lm = R;
+  if (e->stream2 && ngrp >= 2) {
+    e->split_group = (ngrp + 1) / 2;
+    int k = 0, rows = 0, lms = 0;
+    for (int m = 0; m < M && k < e->split_group; ++m) {
+      if (!grp_rows[m]) continue;
+      rows += grp_rows[m];
+      lms += grp_lm[m];
+      ++k;
+    }
+    e->split_row = rows;
+    e->split_lm = lms;
+  }
+  const int sr = e->split_row;
+  // Launch order of the decode-attention items, per stream: full-length key
+  // ranges first, then the shorter ones by decreasing length, so the grid
+  // ends on its shortest workgroups. Every item writes its own partial slot
+  // (or its row's output), so the order changes no result.
+  std::stable_sort(e->items.begin(), e->items.end(), [sr](const AttnItem& a, const AttnItem& b) {
+    const bool sa = a.row >= sr, sb = b.row >= sr;
+    if (sa != sb) return sb;
+    return a.k1 - a.k0 > b.k1 - b.k0;
+  });
   // the split combine in the same spirit: rows with the most partial slots first
-  std::stable_sort(e->red.begin(), e->red.end(),
-                   [](const ReduceItem& a, const ReduceItem& b) { return a.nslots > b.nslots; });
+  std::stable_sort(e->red.begin(), e->red.end(), [sr](const ReduceItem& a, const ReduceItem& b) {
+    const bool sa = a.row >= sr, sb = b.row >= sr;
+    if (sa != sb) return sb;
+    return a.nslots > b.nslots;
+  });
+  e->split_item = 0;
+  e->split_red = 0;
+  e->split_pre = 0;
+  for (const AttnItem& it : e->items) e->split_item += it.row < sr;
+  for (const ReduceItem& rd : e->red) e->split_red += rd.row < sr;
+  for (const PrefillItem& pi : e->pitems) e->split_pre += pi.row0 < sr;   // pushed in row order
   if (!e->plan_only) {
     if (T > e->lay.Tmax || R > e->lay.Rmax || nslots > e->lay.slots_cap ||
         (int64_t)e->items.size() > e->lay.items_cap) {

@@ -147,6 +147,25 @@ def test_bf16_small_ragged_batch():
         say(f"bf16 small req{i} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
 
 
+def test_bf16_four_models_two_streams():
+    """bf16, four models with uneven shares of ragged requests: each step's
+    model groups are split over two streams (two groups and one or two
+    groups), with chunked prefill rows that emit no token beside decode rows
+    past one split, so both streams carry every kernel and the final norm
+    gathers rows from both streams' partials."""
+    consts = EngineConsts(num_kv_blocks=512, max_num_seqs=12, max_prefill_tokens=96, max_model_len=512)
+    ws = [generate_weights(SMALL_BF16, "bf16", 6, 99, m) for m in range(4)]
+    lens = [1, 17, 70, 300, 33, 128, 250, 5, 64, 190]
+    models = [0, 0, 1, 2, 3, 3, 1, 2, 0, 3]
+    Gs = [30, 12, 25, 8, 40, 3, 20, 33, 6, 15]
+    prompts = _prompts(SMALL_BF16.vocab, lens, 6)
+    reqs = [(p, m, G) for p, m, G in zip(prompts, models, Gs)]
+    toks, logs = run_requests(SMALL_BF16, "bf16", consts, ws, reqs)
+    for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
+        err, flips = compare(SMALL_BF16, ws[m], p, t, lg, True, 2e-2, what=f"req{i}")
+        say(f"bf16 four models req{i} model {m} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+
+
 def test_bf16_runs_are_deterministic():
     consts = EngineConsts(num_kv_blocks=256, max_num_seqs=8, max_prefill_tokens=96, max_model_len=512)
     ws = [generate_weights(SMALL_BF16, "bf16", 4, 99, m) for m in range(2)]
