@@ -25,11 +25,16 @@ constexpr int kStageSlots = 4;    // steps that may be in flight (pinned staging
 constexpr int kTargetWaves = 4096;
 constexpr int kBigMinRows = 256;    // a row group this large goes to the 32x32-MFMA GEMM
 constexpr int kBigTargetWgs = 256;  // one workgroup per CU
-// bf16 steps with several models run them on this many streams (the step's
-// model groups split in two halves, the second half on a stream forked from
-// the caller's and joined at the end of the step), so one half's
-// launch-bound kernels and grid tails overlap the other half's work
+// bf16 steps with several models run them on up to this many streams: the
+// step's model groups are dealt out in contiguous shares, the first on the
+// caller's stream, the others on streams forked from it and joined before
+// the final norm, so one share's launch-bound kernels and grid tails overlap
+// the others' work. Two is the measured best on the 4x1B batch: 19.9k tok/s
+// on one stream, 20.8k on two, 19.7k on three, 14.2k on four (more streams
+// than the process's hardware queues serialise).
 constexpr int kModelStreams = 2;
+constexpr int kMaxShares = 4;
+static_assert(kModelStreams >= 1 && kModelStreams <= kMaxShares, "model streams");
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -103,7 +108,8 @@ struct Layout {
   size_t esz;
   int64_t Tmax, Rmax, slots_cap, items_cap, red_cap, part_cap;
   size_t model_bytes, kv_bytes, block_bytes;
-  size_t off_kv, off_tok, off_bt, off_rope, off_meta, off_x, off_xn, off_part, off_part2, off_q, off_ao, off_h,
+  size_t off_xpart[kMaxShares - 1];   // split-K partials of shares 1.. (0: none)
+  size_t off_kv, off_tok, off_bt, off_rope, off_meta, off_x, off_xn, off_part, off_q, off_ao, off_h,
       off_logits, off_pacc, off_pml, off_models, total;
   int64_t token_store, block_store, meta_ints;
 };
@@ -165,9 +171,10 @@ Layout make_layout(const moa_engine_cfg& c) {
   // GEMM inputs (xn, ao, h) hold two planes: bf16 hi and lo (fp32 mode uses the first)
   L.off_xn = take((size_t)2 * L.Tmax * d * L.esz);
   L.off_part = take((size_t)L.part_cap * 4);
-  // the second model stream's split-K partials (its projections run while
-  // the first stream's, of another width, are in flight)
-  L.off_part2 = (c.dtype == MOA_BF16 && kModelStreams > 1 && c.max_models > 1) ? take((size_t)L.part_cap * 4) : 0;
+  // every further share's own split-K partials (its projections run while
+  // another share's, of another width, are in flight)
+  const int nx = (c.dtype == MOA_BF16) ? std::min(kModelStreams, (int)c.max_models) - 1 : 0;
+  for (int k = 0; k < kMaxShares - 1; ++k) L.off_xpart[k] = k < nx ? take((size_t)L.part_cap * 4) : 0;
   L.off_q = take((size_t)L.Tmax * nh * hd * 4);
   L.off_ao = take((size_t)2 * L.Tmax * nh * hd * L.esz);
   L.off_h = take((size_t)2 * L.Tmax * F * L.esz);
@@ -189,8 +196,10 @@ struct moa_engine {
   bool broken = false;
   hipStream_t stream = nullptr;
   hipStream_t copy_stream = nullptr;
-  hipStream_t stream2 = nullptr;      // second model stream (bf16, several models)
-  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
+  int nstreams = 1;                   // model streams: the caller's + xs[0 .. nstreams - 2]
+  hipStream_t xs[kMaxShares - 1] = {};
+  hipEvent_t ev_fork = nullptr;
+  hipEvent_t ev_join[kMaxShares - 1] = {};
   char* arena = nullptr;
   size_t arena_bytes = 0;
   size_t model_top = 0;
@@ -215,7 +224,7 @@ struct moa_engine {
   float* x = nullptr;
   void* xn = nullptr;
   float* part = nullptr;
-  float* part2 = nullptr;             // second model stream's partials
+  float* xpart[kMaxShares - 1] = {};  // partials of shares 1..
   float* q = nullptr;
   void* ao = nullptr;
   void* h = nullptr;
@@ -246,10 +255,12 @@ struct moa_engine {
   std::vector<AttnItem> items;
   std::vector<ReduceItem> red;
   std::vector<PrefillItem> pitems;
-  // the second stream's share of the step: its first model group, row and
-  // LM row, and where its items start (each list holds the first stream's
-  // items first); split_group == number of groups: one stream
-  int split_group = 0, split_row = 0, split_lm = 0, split_item = 0, split_red = 0, split_pre = 0;
+  // the step's shares: share u holds model groups [sh_group[u], sh_group[u+1]),
+  // rows, LM rows and attention / combine / prefill items likewise (each item
+  // list sorted by share first)
+  int nshare = 1;
+  int sh_group[kMaxShares + 1] = {}, sh_row[kMaxShares + 1] = {}, sh_lm[kMaxShares + 1] = {};
+  int sh_item[kMaxShares + 1] = {}, sh_red[kMaxShares + 1] = {}, sh_pre[kMaxShares + 1] = {};
 };
 
 namespace {
@@ -529,7 +540,7 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
     e->x = (float*)(A + L.off_x);
     e->xn = A + L.off_xn;
     e->part = (float*)(A + L.off_part);
-    e->part2 = L.off_part2 ? (float*)(A + L.off_part2) : nullptr;
+    for (int k = 0; k < kMaxShares - 1; ++k) e->xpart[k] = L.off_xpart[k] ? (float*)(A + L.off_xpart[k]) : nullptr;
     e->q = (float*)(A + L.off_q);
     e->ao = A + L.off_ao;
     e->h = A + L.off_h;
@@ -538,10 +549,11 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
     e->pml = (float*)(A + L.off_pml);
     hipError_t err = hipStreamCreateWithFlags(&e->copy_stream, hipStreamNonBlocking);
     for (int i = 0; i < kStageSlots && err == hipSuccess; ++i) err = hipEventCreateWithFlags(&e->ev[i], hipEventDisableTiming);
-    if (err == hipSuccess && e->part2) {
-      err = hipStreamCreateWithFlags(&e->stream2, hipStreamNonBlocking);
-      if (err == hipSuccess) err = hipEventCreateWithFlags(&e->ev_fork, hipEventDisableTiming);
-      if (err == hipSuccess) err = hipEventCreateWithFlags(&e->ev_join, hipEventDisableTiming);
+    if (err == hipSuccess && e->xpart[0]) err = hipEventCreateWithFlags(&e->ev_fork, hipEventDisableTiming);
+    for (int k = 0; k < kMaxShares - 1 && err == hipSuccess && e->xpart[k]; ++k) {
+      err = hipStreamCreateWithFlags(&e->xs[k], hipStreamNonBlocking);
+      if (err == hipSuccess) err = hipEventCreateWithFlags(&e->ev_join[k], hipEventDisableTiming);
+      if (err == hipSuccess) e->nstreams = k + 2;
     }
     if (err == hipSuccess) {
       // RoPE table: angle pos * theta^(-2i/hd) and its cos/sin in double, stored as fp32.
@@ -569,7 +581,8 @@ void moa_destroy(moa_engine* e) {
   if (!e) return;
   if (!e->plan_only) {
     if (e->stream) (void)hipStreamSynchronize(e->stream);
-    if (e->stream2) (void)hipStreamSynchronize(e->stream2);
+    for (hipStream_t x : e->xs)
+      if (x) (void)hipStreamSynchronize(x);
     for (int i = 0; i < kStageSlots; ++i) {
       if (e->stage[i].buf) (void)hipHostFree(e->stage[i].buf);
       if (e->ev[i]) (void)hipEventDestroy(e->ev[i]);
@@ -578,9 +591,11 @@ void moa_destroy(moa_engine* e) {
     for (auto& t : e->timed) { (void)hipEventDestroy(t.a); (void)hipEventDestroy(t.b); }
     for (hipEvent_t v : e->ev_pool) (void)hipEventDestroy(v);
     if (e->copy_stream) (void)hipStreamDestroy(e->copy_stream);
-    if (e->stream2) (void)hipStreamDestroy(e->stream2);
+    for (hipStream_t x : e->xs)
+      if (x) (void)hipStreamDestroy(x);
+    for (hipEvent_t v : e->ev_join)
+      if (v) (void)hipEventDestroy(v);
     if (e->ev_fork) (void)hipEventDestroy(e->ev_fork);
-    if (e->ev_join) (void)hipEventDestroy(e->ev_join);
   }
   delete e;
 }
@@ -928,21 +943,20 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
     int prev_split;
     size_t prev_stride;
   };
-  const int nshare = e->split_group < gin.ngroups ? 2 : 1;
-  Share sh[2];
+  const int nshare = e->nshare;
+  Share sh[kMaxShares];
   for (int u = 0; u < nshare; ++u) {
     Share& b = sh[u];
-    const bool first = u == 0;
-    b.st = first ? e->stream : e->stream2;
-    b.part = first ? e->part : e->part2;
-    b.r0 = first ? 0 : e->split_row;
-    b.nr = first ? e->split_row : T - e->split_row;
-    b.g0 = first ? 0 : e->split_group;
-    b.ng = first ? e->split_group : gin.ngroups - e->split_group;
-    const int i0 = first ? 0 : e->split_item, d0 = first ? 0 : e->split_red, p0 = first ? 0 : e->split_pre;
-    b.nitems = first ? e->split_item : nitems - e->split_item;
-    b.nred = first ? e->split_red : nred - e->split_red;
-    b.npre = first ? e->split_pre : npre - e->split_pre;
+    b.st = u == 0 ? e->stream : e->xs[u - 1];
+    b.part = u == 0 ? e->part : e->xpart[u - 1];
+    b.r0 = e->sh_row[u];
+    b.nr = e->sh_row[u + 1] - e->sh_row[u];
+    b.g0 = e->sh_group[u];
+    b.ng = e->sh_group[u + 1] - e->sh_group[u];
+    const int i0 = e->sh_item[u], d0 = e->sh_red[u], p0 = e->sh_pre[u];
+    b.nitems = e->sh_item[u + 1] - i0;
+    b.nred = e->sh_red[u + 1] - d0;
+    b.npre = e->sh_pre[u + 1] - p0;
     b.items = sd.items + i0;
     b.red = sd.red + d0;
     b.pre = sd.pre + p0;
@@ -976,10 +990,8 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   double gb = 0, gf = 0;
 
   if (T > 0) {
-    if (nshare > 1) {
-      HIPCHK(hipEventRecord(e->ev_fork, s), "stream fork");
-      HIPCHK(hipStreamWaitEvent(e->stream2, e->ev_fork, 0), "stream fork");
-    }
+    if (nshare > 1) HIPCHK(hipEventRecord(e->ev_fork, s), "stream fork");
+    for (int u = 1; u < nshare; ++u) HIPCHK(hipStreamWaitEvent(e->xs[u - 1], e->ev_fork, 0), "stream fork");
     for (int u = 0; u < nshare; ++u) {
       const Share& b = sh[u];
       LAUNCH(MOA_K_EMBED, (double)b.nr * d * (4.0 + esz), 0,
@@ -1050,12 +1062,12 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
         b.prev_stride = ga.out_split;
       }
     }
-    // The final norm, LM head and argmax run on the caller's stream once both
-    // shares are done: their rows are numbered in LM order, which overlaps
-    // the other share's rows in xn and in the partials.
-    if (nshare > 1) {
-      HIPCHK(hipEventRecord(e->ev_join, e->stream2), "stream join");
-      HIPCHK(hipStreamWaitEvent(s, e->ev_join, 0), "stream join");
+    // The final norm, LM head and argmax run on the caller's stream once
+    // every share is done: their rows are numbered in LM order, which
+    // overlaps other shares' rows in xn.
+    for (int u = 1; u < nshare; ++u) {
+      HIPCHK(hipEventRecord(e->ev_join[u - 1], e->xs[u - 1]), "stream join");
+      HIPCHK(hipStreamWaitEvent(s, e->ev_join[u - 1], 0), "stream join");
     }
     if (R > 0) {
       // every share's last down projection was planned over the whole step:
@@ -1063,7 +1075,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
       const int prev_split = sh[0].prev_split;
       const size_t prev_stride = sh[0].prev_stride;
       for (int u = 0; u < nshare; ++u) {
-        const int b0 = u == 0 ? 0 : e->split_lm, nb = u == 0 ? e->split_lm : R - e->split_lm;
+        const int b0 = e->sh_lm[u], nb = e->sh_lm[u + 1] - e->sh_lm[u];
         if (nb == 0) continue;
         LAUNCH(MOA_K_NORM, (double)nb * d * (12.0 + prev_split * 4.0), 0,
                launch_add_rmsnorm(s, bf, e->x, sh[u].part, prev_split, prev_stride, sd.lm_src + b0, sd.row_model, nb,
@@ -1206,47 +1218,54 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
     }
   }
   const int R = (int)e->l_src.size();
-  // Streams: the first half of the step's model groups (rows [0, split_row))
-  // on the caller's stream, the rest on the second stream.
+  // Shares: the step's model groups dealt out in contiguous runs, one per
+  // model stream (rows, LM rows and items follow their groups).
   int ngrp = 0;
   for (int m = 0; m < M; ++m) ngrp += grp_rows[m] > 0;
-  e->split_group = ngrp;
-  e->split_row = T;
-  e->split_lm = R;
-  if (e->stream2 && ngrp >= 2) {
-    e->split_group = (ngrp + 1) / 2;
-    int k = 0, rows = 0, lms = 0;
-    for (int m = 0; m < M && k < e->split_group; ++m) {
+  const int nshare = std::max(1, std::min(e->nstreams, ngrp));
+  e->nshare = nshare;
+  for (int u = 0; u <= nshare; ++u) e->sh_group[u] = (u * ngrp + nshare - 1) / nshare;
+  {
+    int u = 0, k = 0, rows = 0, lms = 0;
+    e->sh_row[0] = 0;
+    e->sh_lm[0] = 0;
+    for (int m = 0; m < M && u < nshare; ++m) {
       if (!grp_rows[m]) continue;
       rows += grp_rows[m];
       lms += grp_lm[m];
       ++k;
+      if (k == e->sh_group[u + 1]) { ++u; e->sh_row[u] = rows; e->sh_lm[u] = lms; }
     }
-    e->split_row = rows;
-    e->split_lm = lms;
+    e->sh_row[nshare] = T;
+    e->sh_lm[nshare] = R;
   }
-  const int sr = e->split_row;
+  const int* shr = e->sh_row;
+  auto share_of = [shr, nshare](int row) { int u = 0; while (u + 1 < nshare && row >= shr[u + 1]) ++u; return u; };
   // Launch order of the decode-attention items, per stream: full-length key
   // ranges first, then the shorter ones by decreasing length, so the grid
   // ends on its shortest workgroups. Every item writes its own partial slot
   // (or its row's output), so the order changes no result.
-  std::stable_sort(e->items.begin(), e->items.end(), [sr](const AttnItem& a, const AttnItem& b) {
-    const bool sa = a.row >= sr, sb = b.row >= sr;
-    if (sa != sb) return sb;
+  std::stable_sort(e->items.begin(), e->items.end(), [&share_of](const AttnItem& a, const AttnItem& b) {
+    const int sa = share_of(a.row), sb = share_of(b.row);
+    if (sa != sb) return sa < sb;
     return a.k1 - a.k0 > b.k1 - b.k0;
   });
   // the split combine in the same spirit: rows with the most partial slots first
-  std::stable_sort(e->red.begin(), e->red.end(), [sr](const ReduceItem& a, const ReduceItem& b) {
-    const bool sa = a.row >= sr, sb = b.row >= sr;
-    if (sa != sb) return sb;
+  std::stable_sort(e->red.begin(), e->red.end(), [&share_of](const ReduceItem& a, const ReduceItem& b) {
+    const int sa = share_of(a.row), sb = share_of(b.row);
+    if (sa != sb) return sa < sb;
     return a.nslots > b.nslots;
   });
-  e->split_item = 0;
-  e->split_red = 0;
-  e->split_pre = 0;
-  for (const AttnItem& it : e->items) e->split_item += it.row < sr;
-  for (const ReduceItem& rd : e->red) e->split_red += rd.row < sr;
-  for (const PrefillItem& pi : e->pitems) e->split_pre += pi.row0 < sr;   // pushed in row order
+  // share boundaries in the item lists (prefill items are pushed in row order)
+  for (int u = 0; u <= nshare; ++u) e->sh_item[u] = e->sh_red[u] = e->sh_pre[u] = 0;
+  for (const AttnItem& it : e->items) e->sh_item[share_of(it.row) + 1]++;
+  for (const ReduceItem& rd : e->red) e->sh_red[share_of(rd.row) + 1]++;
+  for (const PrefillItem& pi : e->pitems) e->sh_pre[share_of(pi.row0) + 1]++;
+  for (int u = 0; u < nshare; ++u) {
+    e->sh_item[u + 1] += e->sh_item[u];
+    e->sh_red[u + 1] += e->sh_red[u];
+    e->sh_pre[u + 1] += e->sh_pre[u];
+  }
   if (!e->plan_only) {
     if (T > e->lay.Tmax || R > e->lay.Rmax || nslots > e->lay.slots_cap ||
         (int64_t)e->items.size() > e->lay.items_cap) {
