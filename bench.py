@@ -40,9 +40,11 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, streams=1):
     """HBM bytes per launch of ``kernel`` from the committed rocprofv3 counter
-    summary, or None when none exists or the kernel source changed since."""
+    summary, or None when none exists, the kernel source changed since, or
+    the counters were taken with another number of model streams (which
+    changes what one launch carries)."""
     import glob
     import hashlib
     src = os.path.join(ROOT, "paper_2606_03014_amd", "csrc", "kernels.hip")
@@ -52,7 +54,8 @@ def measured_traffic(kernel):
             line = line.strip()
             if line.startswith("{") and '"traffic_bytes_per_launch"' in line:
                 rec = json.loads(line)
-                if rec.get("kernel") == kernel and rec.get("kernels_source_sha256_16") == sha:
+                if (rec.get("kernel") == kernel and rec.get("kernels_source_sha256_16") == sha
+                        and rec.get("model_streams", 1) == streams):
                     return rec["traffic_bytes_per_launch"]
     return None
 
@@ -129,7 +132,7 @@ def cpu_baseline_history(cfg, seed, weights0, budget_s):
                        f"fp64 numpy oracle with a KV cache")}
 
 
-def kernel_summary(stats, label=""):
+def kernel_summary(stats, label="", streams=1):
     """Log per-class shares and rates; return the roofline object of the
     class with the largest timed share (None when nothing was timed)."""
     total_timed = sum(s["ms"] for s in stats.values())
@@ -149,7 +152,7 @@ def kernel_summary(stats, label=""):
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(dom_name)
+    roof["traffic"] = measured_traffic(dom_name, streams)
     roof["kernel"] = dom_name
     roof["launches_timed"] = dom["launches"]
     roof["us_per_launch"] = dom["ms"] / max(dom["launches"], 1) * 1e3
@@ -478,6 +481,9 @@ def main():
                          "priced by a per-step cost model (no GPU)")
     ap.add_argument("--window", type=int, default=None,
                     help="submission window of the feeder (default: every expert call up front)")
+    ap.add_argument("--one-stream", action="store_true",
+                    help="run every kernel on one stream (default: a several-model batch splits its "
+                         "models over two overlapping streams)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 8 times (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -510,7 +516,8 @@ def main():
         return
     straggler = cfg.name.startswith("straggler")
     n_models = cfg.n_experts + (1 if cfg.aggregator else 0)
-    eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models)
+    eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models, one_stream=args.one_stream)
+    streams = 1 if (args.one_stream or n_models < 2 or cfg.dtype != "bf16") else 2
     log(f"[bench] {cfg.name}: {n_models} model(s); arena {eng.arena_bytes / 2**30:.1f} GiB")
     mids, weights0 = load_models(eng, cfg, args.seed, n_models)
     read_bps, mfma_fps = eng.measure_peaks()
@@ -518,7 +525,12 @@ def main():
     run = bench_straggler if straggler else bench_feeder
     tokens, wall, config, extra, wl = run(args, cfg, eng, mids)
     stats = eng.kernel_stats()
-    roof = kernel_summary(stats)
+    roof = kernel_summary(stats, streams=streams)
+    config["model_streams"] = streams
+    if roof is not None and streams > 1:
+        roof["overlap"] = ("launch durations from two model streams whose kernels run concurrently: "
+                           "each launch carries half the batch's models and shares the GPU with the "
+                           "other stream's launches (--one-stream times them alone)")
     run_roof_ms = sum(s["roof_ms_all"] for s in stats.values())
     # kernel time of every launch, estimated from the timed sample of each class
     busy_ms = sum(s["ms"] / s["launches"] * s["launches_all"] for s in stats.values() if s["launches"])

@@ -22,7 +22,12 @@
  *     sub-allocates weights, the KV pool and its workspace inside it and never
  *     calls hipMalloc after moa_create; the arena and the stream must outlive
  *     the engine;
- *   - all device work is enqueued on the caller's stream;
+ *   - device work is enqueued on the caller's stream; a bf16 engine with
+ *     max_models > 1 also runs part of a step's layers on one internal stream
+ *     that waits for the caller's stream when the step starts and that the
+ *     caller's stream waits for before the step's final norm and LM head, so
+ *     the caller's stream still orders every step (MOA_FLAG_ONE_STREAM keeps
+ *     everything on the caller's stream);
  *   - single host thread: an engine is not thread-safe;
  *   - after MOA_EHIP only moa_destroy is valid on that engine.
  */
@@ -52,7 +57,15 @@ enum {
   /* Scheduler dry run: every call does its host bookkeeping but no device
    * work is enqueued and no tokens are computed (collected tokens read -1).
    * dev_arena and hip_stream may be NULL. */
-  MOA_FLAG_PLAN_ONLY = 1
+  MOA_FLAG_PLAN_ONLY = 1,
+  /* Run every kernel on the caller's stream. By default a bf16 engine with
+   * several models splits each step's model groups in two halves and runs
+   * the second half's layers on an internal stream (its own split-K
+   * workspace in the arena), so the halves' kernels overlap. Every launch
+   * is planned over the whole step either way, so the results are
+   * bit-identical; the flag gives launch durations that are not shared with
+   * concurrent kernels. */
+  MOA_FLAG_ONE_STREAM = 2
 };
 
 /* Decoder geometry (Llama-style pre-norm decoder: RMSNorm, GQA attention with
@@ -224,7 +237,8 @@ enum {
  * per (query head, query, visible key). */
 typedef struct {
   int64_t launches;   /* timed launches (sampled steps) */
-  double ms;          /* their summed durations (HIP events on the engine's stream) */
+  double ms;          /* their summed durations (HIP events on the launch's stream; with two
+                         model streams a launch may share the GPU with the other stream's) */
   double bytes;       /* their algorithmic bytes */
   double flops;       /* their algorithmic flops */
   int64_t launches_all; /* every launch since the reset */

@@ -173,7 +173,8 @@ Layout make_layout(const moa_engine_cfg& c) {
   L.off_part = take((size_t)L.part_cap * 4);
   // every further share's own split-K partials (its projections run while
   // another share's, of another width, are in flight)
-  const int nx = (c.dtype == MOA_BF16) ? std::min(kModelStreams, (int)c.max_models) - 1 : 0;
+  const int nx = (c.dtype == MOA_BF16 && !(c.flags & MOA_FLAG_ONE_STREAM))
+                     ? std::min(kModelStreams, (int)c.max_models) - 1 : 0;
   for (int k = 0; k < kMaxShares - 1; ++k) L.off_xpart[k] = k < nx ? take((size_t)L.part_cap * 4) : 0;
   L.off_q = take((size_t)L.Tmax * nh * hd * 4);
   L.off_ao = take((size_t)2 * L.Tmax * nh * hd * L.esz);

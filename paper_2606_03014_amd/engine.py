@@ -21,20 +21,22 @@ def model_cfg(shape):
                            shape.head_dim, shape.ffn_dim, shape.vocab, shape.rope_theta, shape.rms_eps)
 
 
-def engine_cfg(shape, dtype, consts, max_models, plan_only=False, token_store=0, block_store=0):
+def engine_cfg(shape, dtype, consts, max_models, plan_only=False, token_store=0, block_store=0,
+               one_stream=False):
+    flags = (M.MOA_FLAG_PLAN_ONLY if plan_only else 0) | (M.MOA_FLAG_ONE_STREAM if one_stream else 0)
     return M.moa_engine_cfg(model_cfg(shape), M.MOA_BF16 if dtype == "bf16" else M.MOA_F32,
                             consts.kv_block_size, consts.num_kv_blocks, consts.max_num_seqs,
                             consts.max_prefill_tokens, consts.max_model_len, max_models,
-                            M.MOA_FLAG_PLAN_ONLY if plan_only else 0, token_store, block_store)
+                            flags, token_store, block_store)
 
 
 class Engine:
     """Owns one moa_engine and (unless plan_only) its torch-allocated arena."""
 
     def __init__(self, shape, dtype, consts, max_models, plan_only=False, device="cuda:0",
-                 token_store=0, block_store=0):
+                 token_store=0, block_store=0, one_stream=False):
         self.shape = shape
-        self.cfg = engine_cfg(shape, dtype, consts, max_models, plan_only, token_store, block_store)
+        self.cfg = engine_cfg(shape, dtype, consts, max_models, plan_only, token_store, block_store, one_stream)
         self.arena_bytes = M.moa_arena_bytes(self.cfg)
         self.plan_only = plan_only
         self.arena = None

@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(_HERE, "libmoa.so")
 MOA_OK, MOA_EINVAL, MOA_ENOMEM, MOA_ENOSPC, MOA_ESTATE, MOA_EHIP = 0, -1, -2, -3, -4, -5
 MOA_F32, MOA_BF16 = 0, 1
 MOA_FLAG_PLAN_ONLY = 1
+MOA_FLAG_ONE_STREAM = 2
 STATUS_NAMES = {0: "MOA_OK", -1: "MOA_EINVAL", -2: "MOA_ENOMEM", -3: "MOA_ENOSPC",
                 -4: "MOA_ESTATE", -5: "MOA_EHIP"}
 

@@ -15,9 +15,9 @@ def say(msg):
     sys.stdout.flush()
 
 
-def run_requests(shape, dtype, consts, weights_list, requests, capture=True, repeat=1):
+def run_requests(shape, dtype, consts, weights_list, requests, capture=True, repeat=1, one_stream=False):
     """requests: [(tokens, model_index, G)]. Returns (tokens by request, logits by request)."""
-    eng = Engine(shape, dtype, consts, len(weights_list))
+    eng = Engine(shape, dtype, consts, len(weights_list), one_stream=one_stream)
     try:
         mids = [eng.load(pack_blob(w, shape)) for w in weights_list]
         outs, caps = [], []

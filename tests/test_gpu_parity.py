@@ -164,6 +164,12 @@ def test_bf16_four_models_two_streams():
     for i, ((p, m, G), t, lg) in enumerate(zip(reqs, toks, logs)):
         err, flips = compare(SMALL_BF16, ws[m], p, t, lg, True, 2e-2, what=f"req{i}")
         say(f"bf16 four models req{i} model {m} P={len(p)} G={G}: max err {err:.2e} flips {flips}")
+    # every launch is planned over the whole step, so one stream gives the same bits
+    toks1, logs1 = run_requests(SMALL_BF16, "bf16", consts, ws, reqs, one_stream=True)
+    for i in range(len(reqs)):
+        assert np.array_equal(toks[i], toks1[i]), f"req{i}: tokens differ between one and two streams"
+        assert np.array_equal(logs[i], logs1[i], equal_nan=True), f"req{i}: logits differ between one and two streams"
+    say("four models: one-stream run bit-identical to the two-stream run")
 
 
 def test_bf16_runs_are_deterministic():
