@@ -110,7 +110,7 @@ struct Layout {
   size_t model_bytes, kv_bytes, block_bytes;
   size_t off_xpart[kMaxShares - 1];   // split-K partials of shares 1.. (0: none)
   size_t off_kv, off_tok, off_bt, off_rope, off_meta, off_x, off_xn, off_part, off_q, off_ao, off_h,
-      off_logits, off_pacc, off_pml, off_models, total;
+      off_logits, off_xl, off_pacc, off_pml, off_models, total;
   int64_t token_store, block_store, meta_ints;
 };
 
@@ -180,6 +180,8 @@ Layout make_layout(const moa_engine_cfg& c) {
   L.off_ao = take((size_t)2 * L.Tmax * nh * hd * L.esz);
   L.off_h = take((size_t)2 * L.Tmax * F * L.esz);
   L.off_logits = take((size_t)L.Rmax * V * 4);
+  // LM-head input (final-norm output in LM-row order; split pair in bf16)
+  L.off_xl = take((size_t)2 * L.Rmax * d * L.esz);
   L.off_pacc = take((size_t)L.slots_cap * nh * hd * 4);
   L.off_pml = take((size_t)L.slots_cap * nh * 2 * 4);
   L.off_models = off;
@@ -230,6 +232,7 @@ struct moa_engine {
   void* ao = nullptr;
   void* h = nullptr;
   float* logits = nullptr;
+  void* xl = nullptr;                 // LM-head input rows (final norm output)
   float* pacc = nullptr;
   float* pml = nullptr;
 
@@ -546,6 +549,7 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
     e->ao = A + L.off_ao;
     e->h = A + L.off_h;
     e->logits = (float*)(A + L.off_logits);
+    e->xl = A + L.off_xl;
     e->pacc = (float*)(A + L.off_pacc);
     e->pml = (float*)(A + L.off_pml);
     hipError_t err = hipStreamCreateWithFlags(&e->copy_stream, hipStreamNonBlocking);
@@ -1063,43 +1067,50 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
         b.prev_stride = ga.out_split;
       }
     }
-    // The final norm, LM head and argmax run on the caller's stream once
-    // every share is done: their rows are numbered in LM order, which
-    // overlaps other shares' rows in xn.
-    for (int u = 1; u < nshare; ++u) {
-      HIPCHK(hipEventRecord(e->ev_join[u - 1], e->xs[u - 1]), "stream join");
-      HIPCHK(hipStreamWaitEvent(s, e->ev_join[u - 1], 0), "stream join");
-    }
+    // Final norm, LM head and argmax of each share's emitting rows, in LM-row
+    // order (the LM head's own input rows and the logits rows are disjoint
+    // across shares), before the join.
     if (R > 0) {
-      // every share's last down projection was planned over the whole step:
-      // same split and stride; the gather reads each row from its share's partials
-      const int prev_split = sh[0].prev_split;
-      const size_t prev_stride = sh[0].prev_stride;
-      for (int u = 0; u < nshare; ++u) {
-        const int b0 = e->sh_lm[u], nb = e->sh_lm[u + 1] - e->sh_lm[u];
-        if (nb == 0) continue;
-        LAUNCH(MOA_K_NORM, (double)nb * d * (12.0 + prev_split * 4.0), 0,
-               launch_add_rmsnorm(s, bf, e->x, sh[u].part, prev_split, prev_stride, sd.lm_src + b0, sd.row_model, nb,
-                                  fill([](const ModelDev& x) { return x.final_norm; }),
-                                  (char*)e->xn + (size_t)b0 * d * L.esz, xn_lo, d, g.rms_eps), "final norm");
-      }
+      const size_t xl_lo = (size_t)L.Rmax * d;
       GemmPlanIn lin;
+      int lmodel[kMaxModels];
       int lr0 = 0;
       for (int m = 0; m < M; ++m) {
         if (grp_lm[m] == 0) continue;
         lin.row0[lin.ngroups] = lr0;
         lin.nrows[lin.ngroups] = grp_lm[m];
         lin.W[lin.ngroups] = e->models[m].lm_head;
+        lmodel[lin.ngroups] = m;
         lr0 += grp_lm[m];
         lin.ngroups++;
       }
-      GemmArgs ga;
-      int mt, nt;
-      plan_gemm(e, lin, 0, lin.ngroups, d, V, EPI_F32, e->xn, xn_lo, e->logits, nullptr, 0, false, ga, mt, nt);
-      gemm_cost(ga, EPI_F32, gb, gf);
-      LAUNCH(MOA_K_GEMM_LMHEAD, gb, gf, launch_gemm(s, bf, ga, EPI_F32, mt, nt), "lm head");
-      LAUNCH(MOA_K_ARGMAX, (double)R * V * 4.0, 0, launch_argmax(s, e->logits, R, V, sd.lm_dst, e->tok_store),
-             "argmax");
+      for (int u = 0; u < nshare; ++u) {
+        const Share& b = sh[u];
+        const int b0 = e->sh_lm[u], nb = e->sh_lm[u + 1] - e->sh_lm[u];
+        if (nb == 0) continue;
+        // the share's LM groups: those of its models, contiguous in model order
+        const int mlo = gmodel[b.g0], mhi = gmodel[b.g0 + b.ng - 1];
+        int lg0 = 0, lng = 0;
+        for (int k = 0; k < lin.ngroups; ++k) {
+          if (lmodel[k] < mlo) lg0 = k + 1;
+          else if (lmodel[k] <= mhi) ++lng;
+        }
+        LAUNCH(MOA_K_NORM, (double)nb * d * (12.0 + b.prev_split * 4.0), 0,
+               launch_add_rmsnorm(b.st, bf, e->x, b.part, b.prev_split, b.prev_stride, sd.lm_src + b0, sd.row_model,
+                                  nb, fill([](const ModelDev& x) { return x.final_norm; }),
+                                  (char*)e->xl + (size_t)b0 * d * L.esz, xl_lo, d, g.rms_eps), "final norm");
+        GemmArgs ga;
+        int mt, nt;
+        plan_gemm(e, lin, lg0, lng, d, V, EPI_F32, e->xl, xl_lo, e->logits, nullptr, 0, false, ga, mt, nt);
+        gemm_cost(ga, EPI_F32, gb, gf);
+        LAUNCH(MOA_K_GEMM_LMHEAD, gb, gf, launch_gemm(b.st, bf, ga, EPI_F32, mt, nt), "lm head");
+        LAUNCH(MOA_K_ARGMAX, (double)nb * V * 4.0, 0,
+               launch_argmax(b.st, e->logits + (size_t)b0 * V, nb, V, sd.lm_dst + b0, e->tok_store), "argmax");
+      }
+    }
+    for (int u = 1; u < nshare; ++u) {
+      HIPCHK(hipEventRecord(e->ev_join[u - 1], e->xs[u - 1]), "stream join");
+      HIPCHK(hipStreamWaitEvent(s, e->ev_join[u - 1], 0), "stream join");
     }
   }
   (void)L;
