@@ -299,7 +299,7 @@ def test_bf16_injected_history_pareto_lengths():
         assert err <= 2e-2
 
 
-@pytest.mark.parametrize("n", [100, 180, 300], ids=["100-rows", "180-rows", "300-rows"])
+@pytest.mark.parametrize("n", [100, 180, 300, 520], ids=["100-rows", "180-rows", "300-rows", "520-rows"])
 def test_bf16_wide_decode_batch(n):
     """A decode batch of n rows of one 8B-width model (two layers): every
     projection and the LM head run as one n-row group. 300 rows take the
@@ -307,13 +307,14 @@ def test_bf16_wide_decode_batch(n):
     phase), 100 rows the workgroup-tile kernel with its widest tiles (64 rows
     x 256 columns), 180 rows both: the square and deep-K projections (o,
     down) on 128-row tiles with a partly empty second tile, the wide ones
-    (qkv, gate-up, LM head) on workgroup tiles. Eight of the calls carry a host K/V history and are
+    (qkv, gate-up, LM head) on workgroup tiles. 520 rows take the
+    128x512 tiles of the large-M GEMM with a partly empty last row tile. Eight of the calls carry a host K/V history and are
     checked teacher-forced against the oracle; the rest have device-filled
     histories and only set the batch shape."""
     from moa_inputs import f32_to_bf16_bits
     from moa_inputs.workload import synthetic_kv
     shape = replace(LLAMA_8B, n_layers=2)
-    consts = EngineConsts(num_kv_blocks=8192, max_num_seqs=512, max_prefill_tokens=64, max_model_len=1024)
+    consts = EngineConsts(num_kv_blocks=16384, max_num_seqs=max(512, n), max_prefill_tokens=64, max_model_len=1024)
     w = generate_weights(LLAMA_8B, "bf16", 5, 4, 0, n_layers=2)
     R = 2
     rng = np.random.default_rng(13)
