@@ -262,6 +262,7 @@ struct moa_engine {
   // the step's shares: share u holds model groups [sh_group[u], sh_group[u+1]),
   // rows, LM rows and attention / combine / prefill items likewise (each item
   // list sorted by share first)
+  int morder[kMaxModels] = {};        // model order of the step's rows
   int nshare = 1;
   int sh_group[kMaxShares + 1] = {}, sh_row[kMaxShares + 1] = {}, sh_lm[kMaxShares + 1] = {};
   int sh_item[kMaxShares + 1] = {}, sh_red[kMaxShares + 1] = {}, sh_pre[kMaxShares + 1] = {};
@@ -899,21 +900,19 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   ModelPtrs mp{};
   auto fill = [&](auto get) { for (int m = 0; m < M; ++m) mp.p[m] = get(e->models[m]); return mp; };
 
+  // one group per model with rows, in the step's row order
   GemmPlanIn gin;
+  int gmodel[kMaxModels];
   int r0 = 0;
-  for (int m = 0; m < M; ++m) {
+  for (int i = 0; i < M; ++i) {
+    const int m = e->morder[i];
     if (grp_rows[m] == 0) continue;
     gin.row0[gin.ngroups] = r0;
     gin.nrows[gin.ngroups] = grp_rows[m];
     gin.W[gin.ngroups] = nullptr;
+    gmodel[gin.ngroups] = m;
     r0 += grp_rows[m];
     gin.ngroups++;
-  }
-  int gmodel[kMaxModels];
-  {
-    int k = 0;
-    for (int m = 0; m < M; ++m)
-      if (grp_rows[m]) gmodel[k++] = m;
   }
   auto weights = [&](auto get) { GemmPlanIn w = gin; for (int k = 0; k < w.ngroups; ++k) w.W[k] = get(e->models[gmodel[k]]); return w; };
 
@@ -1073,28 +1072,24 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
     if (R > 0) {
       const size_t xl_lo = (size_t)L.Rmax * d;
       GemmPlanIn lin;
-      int lmodel[kMaxModels];
+      int lfirst[kMaxModels + 1];     // LM groups of row groups [0, k): lfirst[k]
       int lr0 = 0;
-      for (int m = 0; m < M; ++m) {
+      for (int k = 0; k < gin.ngroups; ++k) {
+        lfirst[k] = lin.ngroups;
+        const int m = gmodel[k];
         if (grp_lm[m] == 0) continue;
         lin.row0[lin.ngroups] = lr0;
         lin.nrows[lin.ngroups] = grp_lm[m];
         lin.W[lin.ngroups] = e->models[m].lm_head;
-        lmodel[lin.ngroups] = m;
         lr0 += grp_lm[m];
         lin.ngroups++;
       }
+      lfirst[gin.ngroups] = lin.ngroups;
       for (int u = 0; u < nshare; ++u) {
         const Share& b = sh[u];
         const int b0 = e->sh_lm[u], nb = e->sh_lm[u + 1] - e->sh_lm[u];
         if (nb == 0) continue;
-        // the share's LM groups: those of its models, contiguous in model order
-        const int mlo = gmodel[b.g0], mhi = gmodel[b.g0 + b.ng - 1];
-        int lg0 = 0, lng = 0;
-        for (int k = 0; k < lin.ngroups; ++k) {
-          if (lmodel[k] < mlo) lg0 = k + 1;
-          else if (lmodel[k] <= mhi) ++lng;
-        }
+        const int lg0 = lfirst[b.g0], lng = lfirst[b.g0 + b.ng] - lg0;
         LAUNCH(MOA_K_NORM, (double)nb * d * (12.0 + b.prev_split * 4.0), 0,
                launch_add_rmsnorm(b.st, bf, e->x, b.part, b.prev_split, b.prev_stride, sd.lm_src + b0, sd.row_model,
                                   nb, fill([](const ModelDev& x) { return x.final_norm; }),
@@ -1176,7 +1171,46 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
       n_dec += 1;
     }
   }
-  // rows grouped by model: prefill chunks then decode rows, each in admission order
+  // Model order of the step's rows. With two model streams the active models
+  // split into two sets of about equal device cost (each model's weights
+  // streamed once, plus the K/V bytes its rows' attention reads) and the rows
+  // are laid out set by set, so each stream's share is one contiguous run.
+  int nfirst = 0;                       // models of the first share (0: even split by count)
+  {
+    double cost[kMaxModels] = {0};
+    bool active[kMaxModels] = {false};
+    const double kv_pos = (double)e->lay.block_bytes / kBlock;   // K/V bytes of one position, all layers
+    for (const Act& a : acts) {
+      const int m = e->reqs[a.id].model;
+      active[m] = true;
+      cost[m] += kv_pos * ((double)a.len * a.start + (double)a.len * (a.len + 1) / 2);
+    }
+    int am[kMaxModels], na = 0, k = 0;
+    double total = 0;
+    for (int m = 0; m < M; ++m)
+      if (active[m]) { cost[m] += (double)e->lay.model_bytes; total += cost[m]; am[na++] = m; }
+    if (e->nstreams == 2 && na >= 2) {
+      unsigned best_mask = 1;
+      double best = 1e300;
+      for (unsigned mask = 1; mask < (1u << na) - 1; mask += 2) {   // the first active model in set one
+        double c1 = 0;
+        for (int i = 0; i < na; ++i)
+          if (mask >> i & 1) c1 += cost[am[i]];
+        const double worst = std::max(c1, total - c1);
+        if (worst < best) { best = worst; best_mask = mask; }
+      }
+      for (int i = 0; i < na; ++i)
+        if (best_mask >> i & 1) e->morder[k++] = am[i];
+      nfirst = k;
+      for (int i = 0; i < na; ++i)
+        if (!(best_mask >> i & 1)) e->morder[k++] = am[i];
+    } else {
+      for (int i = 0; i < na; ++i) e->morder[k++] = am[i];
+    }
+    for (int m = 0; m < M; ++m)
+      if (!active[m]) e->morder[k++] = m;
+  }
+  // rows grouped by model in that order: prefill chunks then decode rows, each in admission order
   const int T = n_pre + n_dec;
   e->r_tok.clear(); e->r_pos.clear(); e->r_bt.clear(); e->r_model.clear();
   e->l_src.clear(); e->l_dst.clear(); e->items.clear(); e->red.clear(); e->pitems.clear();
@@ -1185,7 +1219,8 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
   int grp_rows[kMaxModels] = {0}, grp_lm[kMaxModels] = {0};
   int nslots = 0;
   std::vector<std::pair<int64_t, int>> capture_rows;   // (request, lm row)
-  for (int m = 0; m < M; ++m) {
+  for (int mi = 0; mi < M; ++mi) {
+    const int m = e->morder[mi];
     for (int pass = 0; pass < 2; ++pass) {
       for (const Act& a : acts) {
         if (a.kind != pass) continue;
@@ -1237,11 +1272,13 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
   const int nshare = std::max(1, std::min(e->nstreams, ngrp));
   e->nshare = nshare;
   for (int u = 0; u <= nshare; ++u) e->sh_group[u] = (u * ngrp + nshare - 1) / nshare;
+  if (nshare == 2 && nfirst > 0) e->sh_group[1] = nfirst;
   {
     int u = 0, k = 0, rows = 0, lms = 0;
     e->sh_row[0] = 0;
     e->sh_lm[0] = 0;
-    for (int m = 0; m < M && u < nshare; ++m) {
+    for (int mi = 0; mi < M && u < nshare; ++mi) {
+      const int m = e->morder[mi];
       if (!grp_rows[m]) continue;
       rows += grp_rows[m];
       lms += grp_lm[m];
