@@ -30,8 +30,9 @@ constexpr int kBigTargetWgs = 256;  // one workgroup per CU
 // caller's stream, the others on streams forked from it and joined before
 // the final norm, so one share's launch-bound kernels and grid tails overlap
 // the others' work. Two is the measured best on the 4x1B batch: 19.9k tok/s
-// on one stream, 20.8k on two, 19.7k on three, 14.2k on four (more streams
-// than the process's hardware queues serialise).
+// on one stream, 20.8k on two, 19.7k on three, 14.2k on four with shares by
+// model index (more streams than the process's hardware queues serialise);
+// with cost-balanced shares 21.4k on two and 20.8k on three.
 constexpr int kModelStreams = 2;
 constexpr int kMaxShares = 4;
 static_assert(kModelStreams >= 1 && kModelStreams <= kMaxShares, "model streams");
@@ -1171,11 +1172,13 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
       n_dec += 1;
     }
   }
-  // Model order of the step's rows. With two model streams the active models
-  // split into two sets of about equal device cost (each model's weights
-  // streamed once, plus the K/V bytes its rows' attention reads) and the rows
-  // are laid out set by set, so each stream's share is one contiguous run.
-  int nfirst = 0;                       // models of the first share (0: even split by count)
+  // Model order of the step's rows. With several model streams the active
+  // models are dealt into one set per stream, largest device cost first to
+  // the cheapest set so far (cost: the model's weights, streamed once, plus
+  // the K/V bytes its rows' attention reads), and the rows are laid out set
+  // by set, so each stream's share is one contiguous run.
+  int set_size[kMaxShares] = {0};
+  int nsets = 1;
   {
     double cost[kMaxModels] = {0};
     bool active[kMaxModels] = {false};
@@ -1186,26 +1189,28 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
       cost[m] += kv_pos * ((double)a.len * a.start + (double)a.len * (a.len + 1) / 2);
     }
     int am[kMaxModels], na = 0, k = 0;
-    double total = 0;
     for (int m = 0; m < M; ++m)
-      if (active[m]) { cost[m] += (double)e->lay.model_bytes; total += cost[m]; am[na++] = m; }
-    if (e->nstreams == 2 && na >= 2) {
-      unsigned best_mask = 1;
-      double best = 1e300;
-      for (unsigned mask = 1; mask < (1u << na) - 1; mask += 2) {   // the first active model in set one
-        double c1 = 0;
-        for (int i = 0; i < na; ++i)
-          if (mask >> i & 1) c1 += cost[am[i]];
-        const double worst = std::max(c1, total - c1);
-        if (worst < best) { best = worst; best_mask = mask; }
+      if (active[m]) { cost[m] += (double)e->lay.model_bytes; am[na++] = m; }
+    nsets = std::max(1, std::min(e->nstreams, na));
+    if (nsets > 1) {
+      int by_cost[kMaxModels];
+      for (int i = 0; i < na; ++i) by_cost[i] = am[i];
+      std::stable_sort(by_cost, by_cost + na, [&cost](int a, int b) { return cost[a] > cost[b]; });
+      int set_of[kMaxModels];
+      double load[kMaxShares] = {0};
+      for (int i = 0; i < na; ++i) {
+        int best = 0;
+        for (int u = 1; u < nsets; ++u)
+          if (load[u] < load[best]) best = u;
+        load[best] += cost[by_cost[i]];
+        set_of[by_cost[i]] = best;
       }
-      for (int i = 0; i < na; ++i)
-        if (best_mask >> i & 1) e->morder[k++] = am[i];
-      nfirst = k;
-      for (int i = 0; i < na; ++i)
-        if (!(best_mask >> i & 1)) e->morder[k++] = am[i];
+      for (int u = 0; u < nsets; ++u)
+        for (int i = 0; i < na; ++i)
+          if (set_of[am[i]] == u) { e->morder[k++] = am[i]; set_size[u]++; }
     } else {
       for (int i = 0; i < na; ++i) e->morder[k++] = am[i];
+      set_size[0] = na;
     }
     for (int m = 0; m < M; ++m)
       if (!active[m]) e->morder[k++] = m;
@@ -1271,8 +1276,8 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
   for (int m = 0; m < M; ++m) ngrp += grp_rows[m] > 0;
   const int nshare = std::max(1, std::min(e->nstreams, ngrp));
   e->nshare = nshare;
-  for (int u = 0; u <= nshare; ++u) e->sh_group[u] = (u * ngrp + nshare - 1) / nshare;
-  if (nshare == 2 && nfirst > 0) e->sh_group[1] = nfirst;
+  e->sh_group[0] = 0;
+  for (int u = 0; u < nshare; ++u) e->sh_group[u + 1] = e->sh_group[u] + set_size[u];
   {
     int u = 0, k = 0, rows = 0, lms = 0;
     e->sh_row[0] = 0;
