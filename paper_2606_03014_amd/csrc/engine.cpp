@@ -1188,9 +1188,17 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
       active[m] = true;
       cost[m] += kv_pos * ((double)a.len * a.start + (double)a.len * (a.len + 1) / 2);
     }
+    // a model's GEMMs take the longer of streaming its weights and their
+    // matrix-core issue, which catches up at ~96 rows (split-bf16 on the
+    // 16x16 MFMA against the measured read rate)
+    int nrow[kMaxModels] = {0};
+    for (const Act& a : acts) nrow[e->reqs[a.id].model] += a.len;
     int am[kMaxModels], na = 0, k = 0;
     for (int m = 0; m < M; ++m)
-      if (active[m]) { cost[m] += (double)e->lay.model_bytes; am[na++] = m; }
+      if (active[m]) {
+        cost[m] += (double)e->lay.model_bytes * std::max(1.0, nrow[m] / 96.0);
+        am[na++] = m;
+      }
     nsets = std::max(1, std::min(e->nstreams, na));
     if (nsets > 1) {
       int by_cost[kMaxModels];
