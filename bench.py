@@ -40,11 +40,11 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
-def measured_traffic(kernel, streams=1):
-    """HBM bytes per launch of ``kernel`` from the committed rocprofv3 counter
-    summary, or None when none exists, the kernel source changed since, or
-    the counters were taken with another number of model streams (which
-    changes what one launch carries)."""
+def measured_traffic(kernel, workload, streams=1):
+    """HBM bytes per launch of ``kernel`` on ``workload`` from the committed
+    rocprofv3 counter summaries, or None when none exists, the kernel source
+    changed since, or the counters were taken with another number of model
+    streams (which changes what one launch carries)."""
     import glob
     import hashlib
     src = os.path.join(ROOT, "paper_2606_03014_amd", "csrc", "kernels.hip")
@@ -55,7 +55,7 @@ def measured_traffic(kernel, streams=1):
             if line.startswith("{") and '"traffic_bytes_per_launch"' in line:
                 rec = json.loads(line)
                 if (rec.get("kernel") == kernel and rec.get("kernels_source_sha256_16") == sha
-                        and rec.get("model_streams", 1) == streams):
+                        and rec.get("workload") == workload and rec.get("model_streams", 1) == streams):
                     return rec["traffic_bytes_per_launch"]
     return None
 
@@ -132,7 +132,7 @@ def cpu_baseline_history(cfg, seed, weights0, budget_s):
                        f"fp64 numpy oracle with a KV cache")}
 
 
-def kernel_summary(stats, label="", streams=1):
+def kernel_summary(stats, workload, label="", streams=1):
     """Log per-class shares and rates; return the roofline object of the
     class with the largest timed share (None when nothing was timed)."""
     total_timed = sum(s["ms"] for s in stats.values())
@@ -152,7 +152,7 @@ def kernel_summary(stats, label="", streams=1):
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = measured_traffic(dom_name, streams)
+    roof["traffic"] = measured_traffic(dom_name, workload, streams)
     roof["kernel"] = dom_name
     roof["launches_timed"] = dom["launches"]
     roof["us_per_launch"] = dom["ms"] / max(dom["launches"], 1) * 1e3
@@ -525,7 +525,7 @@ def main():
     run = bench_straggler if straggler else bench_feeder
     tokens, wall, config, extra, wl = run(args, cfg, eng, mids)
     stats = eng.kernel_stats()
-    roof = kernel_summary(stats, streams=streams)
+    roof = kernel_summary(stats, cfg.name, streams=streams)
     config["model_streams"] = streams
     if roof is not None and streams > 1:
         roof["overlap"] = ("launch durations from two model streams whose kernels run concurrently: "
