@@ -40,6 +40,38 @@ def test_library_exports_every_declared_symbol():
     assert declared == set(M.exported_symbols())
 
 
+def test_binding_constants_match_the_header():
+    """Every MOA_* enum value the header defines has the same value in the
+    ctypes binding (flags, dtypes, status codes)."""
+    hdr = open(os.path.join(ROOT, "include", "moa.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    consts = {k: int(v) for k, v in re.findall(r"\b(MOA_[A-Z0-9_]+)\s*=\s*(-?\d+)", hdr)}
+    for name in ("MOA_FLAG_PLAN_ONLY", "MOA_FLAG_ONE_STREAM", "MOA_F32", "MOA_BF16", "MOA_OK", "MOA_EINVAL"):
+        assert name in consts, name
+    for name, value in consts.items():
+        if hasattr(M, name):
+            assert getattr(M, name) == value, name
+    assert consts["MOA_FLAG_PLAN_ONLY"] & consts["MOA_FLAG_ONE_STREAM"] == 0
+
+
+def test_second_model_stream_reserves_one_partial_buffer():
+    """A bf16 engine reserves split-K partials for its second model stream in
+    the arena; MOA_FLAG_ONE_STREAM drops exactly that buffer, and fp32
+    engines (one stream) are unaffected by the flag."""
+    from paper_2606_03014_amd.engine import engine_cfg
+    c = CONFIGS["moa-4x1b-bf16"]
+    two = M.moa_arena_bytes(engine_cfg(c.model, "bf16", c.engine, 4))
+    one = M.moa_arena_bytes(engine_cfg(c.model, "bf16", c.engine, 4, one_stream=True))
+    g, e = c.model, c.engine
+    qkv = (g.n_heads + 2 * g.n_kv_heads) * g.head_dim
+    tmax = e.max_prefill_tokens + e.max_num_seqs
+    part = max(tmax, 8 * e.max_num_seqs) * max(qkv, g.d_model) * 4
+    assert two - one == (part + 255) // 256 * 256
+    f = CONFIGS["tiny-moa-fp32"]
+    assert (M.moa_arena_bytes(engine_cfg(f.model, "f32", f.engine, 3))
+            == M.moa_arena_bytes(engine_cfg(f.model, "f32", f.engine, 3, one_stream=True)))
+
+
 def test_status_strings():
     for code in (0, -1, -2, -3, -4, -5):
         assert M.moa_status_str(code).startswith(M.STATUS_NAMES[code])
