@@ -172,9 +172,13 @@ __global__ __launch_bounds__(256) void k_embed(const int* __restrict__ tok_store
 // ------------------------------------------------- residual add + RMSNorm
 // x[r] += sum_s part[s][r] (split-K partial sums of the previous projection),
 // out[j] = x[r] * rsqrt(mean(x[r]^2) + eps) * gamma, r = gather ? gather[j] : j.
-// One workgroup per row, one float4 of the row per thread (blockDim = d/4);
-// the partial-sum loads of a thread are all in flight before they are added.
-template <bool BF>
+// One workgroup per row, V4 float4s of the row per thread, thread t owning
+// float4s t, t + blockDim, ...: two per thread when d is a multiple of 2048
+// (256 threads at d = 2048, 512 at 4096: the smaller workgroup finds room
+// beside another stream's kernels sooner, and at 4096 it is as fast alone),
+// else one (d / 4 threads, at most 1024).
+// The partial-sum loads of a thread are all in flight before they are added.
+template <bool BF, int V4>
 __global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, const float* __restrict__ part,
                                                       int nsplit, size_t split_stride,
                                                       const int* __restrict__ gather,
@@ -183,32 +187,43 @@ __global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, con
   __shared__ float red[16];
   const int j = blockIdx.x;
   const int r = gather ? gather[j] : j;
-  const int i = threadIdx.x * 4;
   // the row's gain is fetched first, so its dependent loads (model id, gain
-  // pointer, four gains) overlap the partial-sum loads instead of following
-  // the block reduction
+  // pointer, gains) overlap the partial-sum loads instead of following the
+  // block reduction
   const void* g = pick(gamma, row_model[r]);
-  float gv[4];
-  if (BF) {
-    const uint2 gb = *(const uint2*)((const uint16_t*)g + i);
-    gv[0] = __uint_as_float(gb.x << 16); gv[1] = __uint_as_float(gb.x & 0xffff0000u);
-    gv[2] = __uint_as_float(gb.y << 16); gv[3] = __uint_as_float(gb.y & 0xffff0000u);
-  } else {
-    const float4 gf = *(const float4*)((const float*)g + i);
-    gv[0] = gf.x; gv[1] = gf.y; gv[2] = gf.z; gv[3] = gf.w;
-  }
-  float4* xr = (float4*)(x + (size_t)r * d + i);
-  float4 v = *xr;
-  if (nsplit) {
-    const float* pp = part + (size_t)r * d + i;
-#pragma unroll 16
-    for (int s = 0; s < nsplit; ++s) {
-      const float4 p = *(const float4*)(pp + (size_t)s * split_stride);
-      v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+  float gv[V4][4];
+#pragma unroll
+  for (int k = 0; k < V4; ++k) {
+    const int i = (threadIdx.x + k * blockDim.x) * 4;
+    if (BF) {
+      const uint2 gb = *(const uint2*)((const uint16_t*)g + i);
+      gv[k][0] = __uint_as_float(gb.x << 16); gv[k][1] = __uint_as_float(gb.x & 0xffff0000u);
+      gv[k][2] = __uint_as_float(gb.y << 16); gv[k][3] = __uint_as_float(gb.y & 0xffff0000u);
+    } else {
+      const float4 gf = *(const float4*)((const float*)g + i);
+      gv[k][0] = gf.x; gv[k][1] = gf.y; gv[k][2] = gf.z; gv[k][3] = gf.w;
     }
-    *xr = v;
   }
-  float ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+  float* xrow = x + (size_t)r * d;
+  float4 v[V4];
+#pragma unroll
+  for (int k = 0; k < V4; ++k) v[k] = *(const float4*)(xrow + (threadIdx.x + k * blockDim.x) * 4);
+  if (nsplit) {
+    const float* prow = part + (size_t)r * d;
+#pragma unroll 8
+    for (int s = 0; s < nsplit; ++s) {
+#pragma unroll
+      for (int k = 0; k < V4; ++k) {
+        const float4 p = *(const float4*)(prow + (size_t)s * split_stride + (threadIdx.x + k * blockDim.x) * 4);
+        v[k].x += p.x; v[k].y += p.y; v[k].z += p.z; v[k].w += p.w;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < V4; ++k) *(float4*)(xrow + (threadIdx.x + k * blockDim.x) * 4) = v[k];
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < V4; ++k) ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
   ss = wave_sum(ss);
   const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
   if ((threadIdx.x & 63) == 0) red[w] = ss;
@@ -216,17 +231,22 @@ __global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, con
   float tot = 0.f;
   for (int k = 0; k < nw; ++k) tot += red[k];
   const float scale = rsqrtf(tot / (float)d + eps);
-  const float y[4] = {v.x * scale * gv[0], v.y * scale * gv[1], v.z * scale * gv[2], v.w * scale * gv[3]};
-  if (BF) {
-    // split-bf16 pairs packed in hardware, one 8-byte store per plane
-    unsigned h01, l01, h23, l23;
-    split_pair(y[0], y[1], h01, l01);
-    split_pair(y[2], y[3], h23, l23);
-    uint16_t* o = (uint16_t*)out + (size_t)j * d + i;
-    *(uint2*)o = make_uint2(h01, h23);
-    *(uint2*)(o + out_lo) = make_uint2(l01, l23);
-  } else {
-    *(float4*)((float*)out + (size_t)j * d + i) = make_float4(y[0], y[1], y[2], y[3]);
+#pragma unroll
+  for (int k = 0; k < V4; ++k) {
+    const int i = (threadIdx.x + k * blockDim.x) * 4;
+    const float y[4] = {v[k].x * scale * gv[k][0], v[k].y * scale * gv[k][1], v[k].z * scale * gv[k][2],
+                        v[k].w * scale * gv[k][3]};
+    if (BF) {
+      // split-bf16 pairs packed in hardware, one 8-byte store per plane
+      unsigned h01, l01, h23, l23;
+      split_pair(y[0], y[1], h01, l01);
+      split_pair(y[2], y[3], h23, l23);
+      uint16_t* o = (uint16_t*)out + (size_t)j * d + i;
+      *(uint2*)o = make_uint2(h01, h23);
+      *(uint2*)(o + out_lo) = make_uint2(l01, l23);
+    } else {
+      *(float4*)((float*)out + (size_t)j * d + i) = make_float4(y[0], y[1], y[2], y[3]);
+    }
   }
 }
 
@@ -1396,14 +1416,21 @@ hipError_t launch_add_rmsnorm(hipStream_t st, bool bf16, float* x, const float* 
                               size_t split_stride, const int* gather, const int* row_model, int nrows,
                               ModelPtrs gamma, void* out, size_t out_lo, int d, float eps) {
   if (nrows <= 0) return hipSuccess;
-  if (d % 256 || d > 4096) return hipErrorInvalidValue;   // one float4 per thread, <= 1024 threads
-  const int threads = d / 4;
-  if (bf16)
-    klaunch(k_add_rmsnorm<true>, dim3(nrows), dim3(threads), st, x, part, nsplit, split_stride, gather, row_model,
-            gamma, out, out_lo, d, eps);
-  else
-    klaunch(k_add_rmsnorm<false>, dim3(nrows), dim3(threads), st, x, part, nsplit, split_stride, gather, row_model,
-            gamma, out, out_lo, d, eps);
+  if (d % 256 || d > 4096) return hipErrorInvalidValue;
+  // V4 float4s per thread (d % 256 == 0: whole waves, at most 1024 threads)
+  const int v4 = (d % 2048 == 0) ? 2 : 1;
+  const int threads = d / (4 * v4);
+  auto go = [&](auto kern) {
+    klaunch(kern, dim3(nrows), dim3(threads), st, x, part, nsplit, split_stride, gather, row_model, gamma, out,
+            out_lo, d, eps);
+  };
+  if (bf16) {
+    if (v4 == 1) go(k_add_rmsnorm<true, 1>);
+    else go(k_add_rmsnorm<true, 2>);
+  } else {
+    if (v4 == 1) go(k_add_rmsnorm<false, 1>);
+    else go(k_add_rmsnorm<false, 2>);
+  }
   return hipGetLastError();
 }
 
