@@ -26,10 +26,10 @@ constexpr int kTargetWaves = 4096;
 constexpr int kBigMinRows = 256;    // a row group this large goes to the 32x32-MFMA GEMM
 constexpr int kBigTargetWgs = 256;  // one workgroup per CU
 // bf16 steps with several models run them on up to this many streams: the
-// step's model groups are dealt out in contiguous shares, the first on the
-// caller's stream, the others on streams forked from it and joined before
-// the final norm, so one share's launch-bound kernels and grid tails overlap
-// the others' work. Two is the measured best on the 4x1B batch: 19.9k tok/s
+// step's models are dealt out in shares of about equal cost (rows laid out
+// share by share), the first on the caller's stream, the others on streams
+// forked from it at the step's start and joined at its end, so one share's
+// launch-bound kernels and grid tails overlap the others' work. Two is the measured best on the 4x1B batch: 19.9k tok/s
 // on one stream, 20.8k on two, 19.7k on three, 14.2k on four with shares by
 // model index (more streams than the process's hardware queues serialise);
 // with cost-balanced shares 21.4k on two and 20.8k on three.
