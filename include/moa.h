@@ -214,6 +214,22 @@ moa_status moa_debug_chunks(moa_engine* e, int64_t request_id, int64_t* out, int
  * finished, free_blocks_after), 6 int64 per step, oldest first. */
 moa_status moa_debug_steps(moa_engine* e, int64_t* out, int64_t cap_steps, int64_t* n_out);
 
+/* How the last moa_step split its models over the model streams (a
+ * MOA_FLAG_PLAN_ONLY bf16 engine plans the split a GPU engine with two
+ * streams would make, so this can be inspected without a GPU).
+ *   *n_shares: shares used, 1 .. 4;
+ *   *n_models: models with rows in the step;
+ *   models[i], i < n_models: those models in the step's row order;
+ *   cost[i]: the split's cost of models[i]: its weight bytes times
+ *     max(1, rows / 96) plus the K/V bytes its rows' attention reads;
+ *   share_models0[u], share_row0[u], share_lm0[u], u <= n_shares: index in
+ *     models, row and LM row where share u starts (the last entries are
+ *     n_models and the step's row and LM-row counts).
+ * share_* hold at least 5 entries, models and cost max_models. */
+moa_status moa_debug_step_shares(moa_engine* e, int32_t* n_shares, int32_t* n_models, int32_t* models,
+                                 double* cost, int32_t* share_models0, int32_t* share_row0,
+                                 int32_t* share_lm0);
+
 /* Capture the fp32 logits row of every token request_id emits: row j (the
  * logits that produced output token j) is copied to host_logits + j * vocab
  * once the step that computes it completes. host_logits must hold

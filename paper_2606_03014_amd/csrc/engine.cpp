@@ -264,6 +264,8 @@ struct moa_engine {
   // rows, LM rows and attention / combine / prefill items likewise (each item
   // list sorted by share first)
   int morder[kMaxModels] = {};        // model order of the step's rows
+  int nactive = 0;                    // models with rows (the first nactive of morder)
+  double mcost[kMaxModels] = {};      // the split's cost per model
   int nshare = 1;
   int sh_group[kMaxShares + 1] = {}, sh_row[kMaxShares + 1] = {}, sh_lm[kMaxShares + 1] = {};
   int sh_item[kMaxShares + 1] = {}, sh_red[kMaxShares + 1] = {}, sh_pre[kMaxShares + 1] = {};
@@ -533,6 +535,8 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
   e->bf16 = cfg->dtype == MOA_BF16;
   e->free_blocks.init(cfg->num_kv_blocks);
   e->model_top = L.off_models;
+  // a dry run plans the model-stream shares a GPU engine would use
+  if (plan_only && L.off_xpart[0]) e->nstreams = 1 + (int)std::count_if(L.off_xpart, L.off_xpart + kMaxShares - 1, [](size_t o) { return o != 0; });
   if (!plan_only) {
     e->stream = (hipStream_t)hip_stream;
     e->arena = (char*)dev_arena;
@@ -1199,6 +1203,8 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
         cost[m] += (double)e->lay.model_bytes * std::max(1.0, nrow[m] / 96.0);
         am[na++] = m;
       }
+    for (int m = 0; m < M; ++m) e->mcost[m] = cost[m];
+    e->nactive = na;
     nsets = std::max(1, std::min(e->nstreams, na));
     if (nsets > 1) {
       int by_cost[kMaxModels];
@@ -1513,6 +1519,25 @@ moa_status moa_debug_kernel_stats(moa_engine* e, moa_kernel_stats* out) {
     if (st != MOA_OK) return st;
   }
   for (int i = 0; i < MOA_K_COUNT; ++i) out[i] = e->kstats[i];
+  return MOA_OK;
+}
+
+moa_status moa_debug_step_shares(moa_engine* e, int32_t* n_shares, int32_t* n_models, int32_t* models,
+                                 double* cost, int32_t* share_models0, int32_t* share_row0,
+                                 int32_t* share_lm0) {
+  if (!e || !n_shares || !n_models || !models || !cost || !share_models0 || !share_row0 || !share_lm0)
+    return MOA_EINVAL;
+  *n_shares = e->nshare;
+  *n_models = e->nactive;
+  for (int i = 0; i < e->nactive; ++i) {
+    models[i] = e->morder[i];
+    cost[i] = e->mcost[e->morder[i]];
+  }
+  for (int u = 0; u <= e->nshare; ++u) {
+    share_models0[u] = e->sh_group[u];
+    share_row0[u] = e->sh_row[u];
+    share_lm0[u] = e->sh_lm[u];
+  }
   return MOA_OK;
 }
 

@@ -90,6 +90,9 @@ class Engine:
     def measure_peaks(self):
         return M.moa_debug_measure_peaks(self.h)
 
+    def step_shares(self):
+        return M.moa_debug_step_shares(self.h, self.cfg.max_models)
+
     def capture_logits(self, rid, arr):
         M.moa_debug_capture_logits(self.h, rid, arr)
 

@@ -80,6 +80,8 @@ _SIGS = {
     "moa_debug_time_kernels": (C.c_int, [C.c_void_p, C.c_int32, C.c_double, C.c_double]),
     "moa_debug_kernel_stats": (C.c_int, [C.c_void_p, P(moa_kernel_stats)]),
     "moa_debug_measure_peaks": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double)]),
+    "moa_debug_step_shares": (C.c_int, [C.c_void_p, P(C.c_int32), P(C.c_int32), P(C.c_int32), P(C.c_double),
+                                        P(C.c_int32), P(C.c_int32), P(C.c_int32)]),
 }
 
 _lib = None
@@ -261,6 +263,22 @@ def moa_debug_kernel_stats(eng):
     check(lib().moa_debug_kernel_stats(eng, out), "moa_debug_kernel_stats")
     return {n: {f: getattr(out[i], f) for f, _ in moa_kernel_stats._fields_}
             for i, n in enumerate(KERNEL_CLASSES)}
+
+
+def moa_debug_step_shares(eng, max_models):
+    """How the last step split its models over the model streams:
+    {"models": [...], "cost": [...], "shares": [(models, rows, lm_rows), ...]}
+    with each share's models as a list and its rows / LM rows as ranges."""
+    ns, nm = C.c_int32(), C.c_int32()
+    models = (C.c_int32 * max_models)()
+    cost = (C.c_double * max_models)()
+    m0, r0, l0 = (C.c_int32 * 5)(), (C.c_int32 * 5)(), (C.c_int32 * 5)()
+    check(lib().moa_debug_step_shares(eng, C.byref(ns), C.byref(nm), models, cost, m0, r0, l0),
+          "moa_debug_step_shares")
+    mods = list(models[:nm.value])
+    shares = [(mods[m0[u]:m0[u + 1]], range(r0[u], r0[u + 1]), range(l0[u], l0[u + 1]))
+              for u in range(ns.value)]
+    return {"models": mods, "cost": list(cost[:nm.value]), "shares": shares}
 
 
 def moa_debug_measure_peaks(eng):

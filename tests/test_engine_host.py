@@ -72,6 +72,69 @@ def test_second_model_stream_reserves_one_partial_buffer():
             == M.moa_arena_bytes(engine_cfg(f.model, "f32", f.engine, 3, one_stream=True)))
 
 
+def test_model_stream_shares_are_greedy_cost_balanced():
+    """A plan-only bf16 engine plans the model-stream split of a two-stream
+    GPU engine. On every step of a skewed four-expert batch: the shares
+    partition the step's models, rows and LM rows into contiguous runs; each
+    model's cost is its weight bytes times max(1, rows / 96) plus the K/V
+    bytes its rows' attention reads; and the split is the greedy one (largest
+    cost first, each to the share with the least cost so far)."""
+    from paper_2606_03014_amd.engine import engine_cfg
+    c = CONFIGS["moa-4x1b-bf16"]
+    g = c.model
+    model_bytes = (M.moa_arena_bytes(engine_cfg(g, "bf16", c.engine, 4))
+                   - M.moa_arena_bytes(engine_cfg(g, "bf16", c.engine, 3)))
+    kv_pos = g.n_layers * g.n_kv_heads * 2 * g.head_dim * 2
+    eng = _dry(g, c.engine, 4)
+    snaps = {}
+    wl = make_workload(c.name, 0, n_queries=48)
+    r = run_feeder(eng, wl, [0, 1, 2, 3], on_step=lambda info: snaps.__setitem__(info.step, eng.step_shares()))
+    S = r.n_steps
+    rows = np.zeros((S, 4), np.int64)
+    lms = np.zeros((S, 4), np.int64)
+    keys = np.zeros((S, 4), np.float64)
+    for (q, m), rid in r.rid_of.items():
+        info = eng.request(rid)
+        P = info.prompt_len
+        for s, a, b in eng.chunks(rid):
+            rows[s, m] += b
+            keys[s, m] += b * a + b * (b + 1) / 2          # positions a .. a+b-1 see pos+1 keys
+            lms[s, m] += (a + b == P)
+        d0 = max(s for s, a, b in eng.chunks(rid)) + 1
+        for t in range(d0, info.finish_step + 1):
+            rows[t, m] += 1
+            lms[t, m] += 1
+            keys[t, m] += P + 1 + (t - d0)
+    eng.close()
+    two = 0
+    for s in range(S):
+        sh = snaps[s]
+        active = [m for m in range(4) if rows[s, m]]
+        assert sorted(sh["models"]) == active
+        assert len(sh["shares"]) == max(1, min(2, len(active)))
+        assert [m for mods, _, _ in sh["shares"] for m in mods] == sh["models"]
+        r0 = l0 = 0
+        for mods, rr, ll in sh["shares"]:
+            assert mods == sorted(mods)
+            assert rr.start == r0 and len(rr) == sum(rows[s, m] for m in mods)
+            assert ll.start == l0 and len(ll) == sum(lms[s, m] for m in mods)
+            r0, l0 = rr.stop, ll.stop
+        assert r0 == rows[s].sum() and l0 == lms[s].sum()
+        cost = dict(zip(sh["models"], sh["cost"]))
+        for m in active:
+            want = model_bytes * max(1.0, rows[s, m] / 96.0) + kv_pos * keys[s, m]
+            assert cost[m] == pytest.approx(want, rel=1e-12)
+        if len(active) >= 2:
+            two += 1
+            load, sets = [0.0, 0.0], [[], []]
+            for m in sorted(active, key=lambda m: -cost[m]):
+                u = 0 if load[0] <= load[1] else 1
+                load[u] += cost[m]
+                sets[u].append(m)
+            assert [sorted(x) for x in sets] == [mods for mods, _, _ in sh["shares"]]
+    assert two > S // 2
+
+
 def test_status_strings():
     for code in (0, -1, -2, -3, -4, -5):
         assert M.moa_status_str(code).startswith(M.STATUS_NAMES[code])
