@@ -1,0 +1,43 @@
+"""bench.py's reading of committed counter records (CPU only)."""
+import hashlib
+import importlib.util
+import json
+import os
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench():
+    spec = importlib.util.spec_from_file_location("bench_under_test", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+def test_traffic_records_match_source_workload_and_streams(tmp_path):
+    """A traffic record applies only to the kernel source it was taken on,
+    its workload and its number of model streams (which set what one launch
+    carries); records without a stream count are one-stream records."""
+    bench = _bench()
+    src = tmp_path / "paper_2606_03014_amd" / "csrc"
+    src.mkdir(parents=True)
+    (src / "kernels.hip").write_bytes(b"// kernels\n")
+    sha = hashlib.sha256(b"// kernels\n").hexdigest()[:16]
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    recs = [
+        {"kernel": "gemm_gateup", "kernels_source_sha256_16": sha, "workload": "w", "model_streams": 2,
+         "traffic_bytes_per_launch": 2.0},
+        {"kernel": "gemm_gateup", "kernels_source_sha256_16": sha, "workload": "w",
+         "traffic_bytes_per_launch": 1.0},
+        {"kernel": "attn", "kernels_source_sha256_16": "0" * 16, "workload": "w", "model_streams": 1,
+         "traffic_bytes_per_launch": 3.0},
+    ]
+    (prof / "traffic_w.md").write_text("# t\n\n```\n" + "\n".join(json.dumps(r) for r in recs) + "\n```\n")
+    (prof / "kernels_w.md").write_text(json.dumps(dict(recs[0], traffic_bytes_per_launch=9.0)) + "\n")
+    bench.ROOT = str(tmp_path)
+    assert bench.measured_traffic("gemm_gateup", "w", 2) == 2.0
+    assert bench.measured_traffic("gemm_gateup", "w", 1) == 1.0
+    assert bench.measured_traffic("gemm_gateup", "other", 2) is None
+    assert bench.measured_traffic("attn", "w", 1) is None          # another kernel source
+    assert bench.measured_traffic("gemm_down", "w", 1) is None
