@@ -502,8 +502,8 @@ def main():
         schedule_study(args, CONFIGS[args.workload])
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); this build has no "
-              "multi-GPU path: the engine runs every model of the batch on one MI355X.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the engine has no "
+              "multi-GPU path: it runs every model of the batch on one MI355X.", file=sys.stderr)
         sys.exit(2)
 
     import torch
