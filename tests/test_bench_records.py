@@ -41,3 +41,14 @@ def test_traffic_records_match_source_workload_and_streams(tmp_path):
     assert bench.measured_traffic("gemm_gateup", "other", 2) is None
     assert bench.measured_traffic("attn", "w", 1) is None          # another kernel source
     assert bench.measured_traffic("gemm_down", "w", 1) is None
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """The engine runs on one GPU: bench.py --gpus 2 exits with status 2 and
+    says so, before touching a GPU."""
+    import subprocess
+    import sys
+    out = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                         capture_output=True, text=True, timeout=120)
+    assert out.returncode == 2
+    assert "one GPU only" in out.stderr and out.stdout == ""
