@@ -1,20 +1,33 @@
 #!/usr/bin/env python3
 """Benchmark: generated tokens/s of a ragged mixture-of-agents batch on one MI355X.
 
-One step = the whole batch: every routed expert call of the workload (and the
-aggregator calls, if the workload has an aggregator) submitted, generated to
-its max_new_tokens and collected through the C ABI. The default workload is
-four Llama-1B-shape experts (bf16, random init) serving 256 queries routed
-top-2 by Zipf(1.2) popularity, with bimodal instruct/reasoning generation
-lengths (512 calls, 541,743 generated tokens at seed 0) -- the skewed,
-straggler-heavy expert phase of the paper (Sections "Motivation" and
-"Workload Characterisation"). Weights, prompts and routing are synthetic.
+The default workload is the paper's own setting (Section "Problem Setting";
+Section "MOSAIC: Adaptive Aggregation"): three expert models and one
+aggregator, all of Llama-8B shape (bf16, random init), co-resident on one GPU
+with one shared paged KV pool. 1,024 queries are routed top-2 by Zipf(1.0)
+popularity, and generation lengths are bimodal (60% instruct-style U[128,
+1024], 40% reasoning-style lognormal with median 4,096 capped at 16,384).
+The aggregator call of a query, on the query followed by its experts'
+outputs, emits 512 tokens. Weights, prompts and routing are synthetic.
 
-Prints one JSON line. The ``roofline`` object covers the kernel class with
-the largest share of the timed region; ``run_roofline`` is the whole run's
-roofline time (sum over every launch of max(bytes/8 TB/s, flops/2.5 PF/s))
-over the measured wall time; ``cpu_baseline`` times the fp64 oracle on a
-bounded sample of the same workload.
+One bench step = a fixed block of ``--block-steps`` consecutive engine steps
+(128 by default) of that workload's deterministic schedule, driven by the
+host feeder from the first submit. The warm-up steps are the schedule's first
+blocks (admission and the initial prefill burst). The timed steps are the
+blocks that follow, a stated window of engine steps of the expert phase with
+aggregator calls arriving. Every token those engine steps emit is counted
+(their decode rows plus the prompts they complete). Nothing is skipped: each
+engine step runs every layer of every row of every model it holds. The whole
+workload takes about 42,000 engine steps, too long for one bench run.
+``--block-steps 0`` makes a bench step the whole batch (other workloads).
+
+Prints one JSON line. ``roofline`` covers the kernel class with the largest
+share of the timed region's kernel time; ``bars`` reports the classes the
+design targets are set on (decode attention and the small/medium-row GEMMs
+against HBM, the large-row GEMMs against bf16 MFMA); ``run_roofline`` is the
+whole run's roofline time (sum over every launch of max(bytes/8 TB/s,
+flops/2.5 PF/s)) over the measured wall time; ``cpu_baseline`` times the fp64
+oracle on a fixed slice of the same workload.
 """
 import argparse
 import json
@@ -34,6 +47,7 @@ METRIC = "generated tokens/s on 1 MI355X (ragged MoA batch); attn/GEMM % of HBM/
 STUDY_BW = 5.0e12
 STUDY_LIN = 4.7e14
 STUDY_ATTN = 3.2e14
+DEFAULT_STREAMS = 2
 
 
 def log(msg):
@@ -60,7 +74,28 @@ def measured_traffic(kernel, workload, streams=1):
     return None
 
 
+def host_cpu():
+    """The host's logical CPUs (nproc), the CPUs this process may run on, and
+    the CPU model name from lscpu."""
+    import subprocess
+    model = None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except Exception:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except Exception:
+        usable = os.cpu_count()
+    return {"nproc": os.cpu_count(), "usable_cpus": usable, "model": model}
+
+
 def oracle_threads():
+    """Threads the oracle's BLAS calls use (its only parallel part)."""
     try:
         from threadpoolctl import threadpool_info
         return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
@@ -68,51 +103,78 @@ def oracle_threads():
         return os.cpu_count()
 
 
-def cpu_baseline(cfg, wl, weights0, budget_s):
-    """The oracle, as it stands, on the workload's first call of model 0 (an
-    expert call, or the first aggregator call when there are no experts):
-    prefill its prompt in chunks of 256 positions (stopping after half the
-    budget if the prompt is that long), then decode until the budget runs out."""
+def upcast_oracle(om, names):
+    """Fill the oracle's float64 weight cache (setup, not timed). One tensor
+    at a time: threads converting several tensors at once ran ten times
+    slower here."""
+    for name in names:
+        om.W(name)
+
+
+CPU_DECODE = 8          # decode steps of the oracle slice
+CPU_PREFILL_MAX = 256   # prompt positions of the oracle slice at most
+
+
+def cpu_baseline(cfg, wl, weights0):
+    """The oracle, as it stands, on a fixed slice of the workload: the first
+    call of model 0 (an expert call, or the first aggregator call when there
+    are no experts). Its prompt (the first CPU_PREFILL_MAX positions of it at
+    most) is prefilled at full depth in one pass, then CPU_DECODE greedy
+    decode steps run with a KV cache; value = the slice's generated tokens /
+    its wall time, on every BLAS thread. The decode steps are timed again on
+    one thread (continuing the same call)."""
     from oracle import transformer as T
     om = T.OracleModel(cfg.model, weights0)
-    for name in weights0:                       # fp64 upcast of the weights: setup, not timed
-        om.W(name)
+    upcast_oracle(om, list(weights0))
     reqs = [r for r in wl.expert_requests() if r[1] == 0]
     q, G = (reqs[0][0], reqs[0][2]) if reqs else (0, wl.agg_max_new)
-    prompt = wl.prompts[q]
+    prompt = wl.prompts[q][:CPU_PREFILL_MAX]
+    D = max(0, min(CPU_DECODE, G - 1))
     kv = T.ContiguousKV(cfg.model.n_layers, cfg.model.n_kv_heads, cfg.model.head_dim)
+    threads = oracle_threads()
     t0 = time.perf_counter()
-    pos = 0
-    while pos < len(prompt):
-        c = min(256, len(prompt) - pos)
-        lg = T.forward_chunk(om, prompt[pos:pos + c], pos, kv, bf16_kv=True, want="last")[-1]
-        pos += c
-        if time.perf_counter() - t0 > budget_s / 2:
-            break
+    lg = T.forward_chunk(om, prompt, 0, kv, bf16_kv=cfg.dtype == "bf16", want="last")[-1]
     t_pre = time.perf_counter() - t0
     toks = [T.argmax_lowest(lg)]
-    while len(toks) < G and time.perf_counter() - t0 < budget_s:
-        lg = T.forward_chunk(om, [toks[-1]], pos + len(toks) - 1, kv, bf16_kv=True)[-1]
+    for _ in range(D):
+        lg = T.forward_chunk(om, [toks[-1]], len(prompt) + len(toks) - 1, kv, bf16_kv=cfg.dtype == "bf16")[-1]
         toks.append(T.argmax_lowest(lg))
     dt = time.perf_counter() - t0
-    return {"value": len(toks) / dt, "unit": "tokens/s", "cores": oracle_threads(), "kind": "oracle",
-            "sample": (f"model-0 call of query {q}: prefill of {pos} of its {len(prompt)} prompt tokens "
-                       f"({t_pre:.1f} s) plus {len(toks) - 1} decode steps ({len(toks)} generated tokens, "
-                       f"{dt:.1f} s, fp64 numpy oracle with a KV cache)")}
+    t_dec = dt - t_pre
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        n1 = 2
+        with threadpool_limits(1):
+            t1 = time.perf_counter()
+            for _ in range(n1):
+                lg = T.forward_chunk(om, [toks[-1]], len(prompt) + len(toks) - 1, kv,
+                                     bf16_kv=cfg.dtype == "bf16")[-1]
+                toks.append(T.argmax_lowest(lg))
+            one = {"decode_tokens_per_s": n1 / (time.perf_counter() - t1), "threads": 1,
+                   "sample": f"{n1} further decode steps of the same call on one BLAS thread"}
+    except Exception as err:            # threadpoolctl missing: say so instead of guessing
+        one = {"unavailable": str(err)}
+    return {"value": (1 + D) / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"the workload's first model-0 call (query {q}): its {len(prompt)}-token prompt "
+                       f"prefilled at full depth in one pass ({t_pre:.1f} s, 1 token), then {D} greedy "
+                       f"decode steps with a KV cache ({t_dec:.1f} s); fp64 numpy oracle, "
+                       f"{1 + D} generated tokens in {dt:.1f} s"),
+            "prefill_s": t_pre, "decode_tokens_per_s": D / t_dec if D else None,
+            "host": host_cpu(), "single_thread": one}
 
 
-def cpu_baseline_history(cfg, seed, weights0, budget_s):
+def cpu_baseline_history(cfg, seed, weights0):
     """The oracle on the straggler workload's first sequence: its synthetic
-    K/V history (bf16-rounded) in a contiguous cache, then decode steps until
-    the budget or its remaining length runs out."""
+    K/V history (bf16-rounded) in a contiguous cache, then CPU_DECODE decode
+    steps (fewer if its remaining length is shorter)."""
     import numpy as np
     from moa_inputs import make_straggler_workload, synthetic_kv, f32_to_bf16_bits
     from moa_inputs.weights import bf16_bits_to_f32
     from oracle import transformer as T
     m = cfg.model
     om = T.OracleModel(m, weights0)
-    for name in weights0:
-        om.W(name)
+    upcast_oracle(om, list(weights0))
     L, tok, R = make_straggler_workload(seed).sequence(0)
     hist = bf16_bits_to_f32(f32_to_bf16_bits(synthetic_kv(seed, 0, m.n_layers, L, m.n_kv_heads, m.head_dim)))
     kv = T.ContiguousKV(m.n_layers, m.n_kv_heads, m.head_dim)
@@ -122,20 +184,24 @@ def cpu_baseline_history(cfg, seed, weights0, budget_s):
     del hist
     t0 = time.perf_counter()
     toks = [tok]
-    while len(toks) <= R and time.perf_counter() - t0 < budget_s:
+    while len(toks) <= min(R, CPU_DECODE):
         lg = T.forward_chunk(om, [toks[-1]], L + len(toks) - 1, kv, bf16_kv=True)[-1]
         toks.append(T.argmax_lowest(lg))
     dt = time.perf_counter() - t0
     n = len(toks) - 1
     return {"value": n / dt, "unit": "tokens/s", "cores": oracle_threads(), "kind": "oracle",
             "sample": (f"sequence 0 (KV history {L} positions, synthetic): {n} decode steps in {dt:.1f} s, "
-                       f"fp64 numpy oracle with a KV cache")}
+                       f"fp64 numpy oracle with a KV cache"), "host": host_cpu()}
 
 
 def kernel_summary(stats, workload, label="", streams=1):
     """Log per-class shares and rates; return the roofline object of the
-    class with the largest timed share (None when nothing was timed)."""
-    total_timed = sum(s["ms"] for s in stats.values())
+    class with the largest timed share (None when nothing was timed). The
+    GEMM views (every GEMM launch counted again by the kernel that ran it)
+    are logged but never chosen and never summed."""
+    from paper_2606_03014_amd.moa import VIEW_CLASSES
+    real = {k: v for k, v in stats.items() if k not in VIEW_CLASSES}
+    total_timed = sum(s["ms"] for s in real.values())
     if total_timed <= 0:
         return None
     for name, s in sorted(stats.items(), key=lambda kv: -kv[1]["ms"]):
@@ -143,22 +209,48 @@ def kernel_summary(stats, workload, label="", streams=1):
             log(f"[bench] {label}{name:12s} {100 * s['ms'] / total_timed:5.1f}% of timed  "
                 f"{s['ms'] / s['launches'] * 1e3:8.1f} us/launch  "
                 f"{s['bytes'] / (s['ms'] * 1e-3) / 1e9:8.1f} GB/s  {s['flops'] / (s['ms'] * 1e-3) / 1e12:7.1f} TF/s")
-    dom_name, dom = max(stats.items(), key=lambda kv: kv[1]["ms"])
-    intensity = dom["flops"] / max(dom["bytes"], 1.0)
-    if intensity > MFMA_BF16_PEAK / HBM_PEAK:
-        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s"}
-    else:
-        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
+    dom_name, dom = max(real.items(), key=lambda kv: kv[1]["ms"])
+    roof = roof_of(dom)
     roof["traffic"] = measured_traffic(dom_name, workload, streams)
     roof["kernel"] = dom_name
     roof["launches_timed"] = dom["launches"]
     roof["us_per_launch"] = dom["ms"] / max(dom["launches"], 1) * 1e3
     roof["algorithmic_bytes_per_launch"] = dom["bytes"] / max(dom["launches"], 1)
     roof["algorithmic_flops_per_launch"] = dom["flops"] / max(dom["launches"], 1)
+    roof["share_of_timed_kernel_time"] = dom["ms"] / total_timed
     return roof
+
+
+def roof_of(s):
+    """Achieved rate of one class against the roof its arithmetic intensity
+    puts it under (HBM below the ridge point, bf16 MFMA above)."""
+    if s["flops"] / max(s["bytes"], 1.0) > MFMA_BF16_PEAK / HBM_PEAK:
+        achieved = s["flops"] / (s["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": MFMA_BF16_PEAK / 1e12, "unit": "TFLOP/s"}
+    else:
+        achieved = s["bytes"] / (s["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    return roof
+
+
+def design_bars(stats):
+    """The classes the design targets are set on, each against its roof:
+    decode attention and the small/medium-row GEMM kernel against 8 TB/s
+    (target 70%), the large-row GEMM kernel against 2.5 PF/s of useful bf16
+    flops (target 60%), and causal prefill attention against 2.5 PF/s."""
+    out = {}
+    for name, bound in (("attn", "hbm"), ("gemm_small_m", "hbm"), ("gemm_large_m", "mfma"),
+                        ("prefill_attn", "mfma")):
+        s = stats.get(name)
+        if not s or not s["launches"] or s["ms"] <= 0:
+            continue
+        sec = s["ms"] * 1e-3
+        frac = s["bytes"] / sec / HBM_PEAK if bound == "hbm" else s["flops"] / sec / MFMA_BF16_PEAK
+        out[name] = {"bound": bound, "frac": round(frac, 4), "launches_timed": s["launches"],
+                     "us_per_launch": round(s["ms"] / s["launches"] * 1e3, 2),
+                     "target": 0.7 if bound == "hbm" else 0.6}
+    return out
 
 
 def class_rates(stats):
@@ -209,17 +301,19 @@ def load_models(eng, cfg, seed, n_models):
 
 
 def bench_feeder(args, cfg, eng, mids):
-    """Every routed expert call (and aggregator call) of the workload, run to
-    completion through the feeder; returns (tokens, seconds, extra)."""
+    """The workload's routed expert calls (and aggregator calls) through the
+    feeder: each bench step is a block of args.block_steps engine steps of
+    the one deterministic schedule (0: the whole batch, from submit to the
+    last collect). Returns (tokens, seconds, config, extra, workload)."""
     import torch
     from moa_inputs import make_workload
-    from paper_2606_03014_amd import run_feeder
+    from paper_2606_03014_amd import Feeder
     wl = make_workload(cfg.name, args.seed, n_queries=args.queries)
     log(f"[bench] {cfg.name}: {wl.n_queries} queries, {len(wl.max_new)} expert calls, "
         f"{sum(len(p) for p in wl.prompts)} query prompt tokens")
     agg = mids[cfg.n_experts] if cfg.aggregator else -1
     prog = Progress()
-    phase = {"prefill_steps": 0, "prefill_tokens": 0, "decode_rows": 0, "steps": 0}
+    phase = {"prefill_steps": 0, "prefill_tokens": 0, "decode_rows": 0, "steps": 0, "models_rows": 0}
 
     def on_step(info):
         prog(info)
@@ -233,43 +327,66 @@ def bench_feeder(args, cfg, eng, mids):
         A = args.answer_options
         gate = dict(gate_tau=args.gate_tau, answer_of=lambda q, e, toks: int(toks[0]) % A)
 
+    def new_feeder():
+        return Feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step, order=args.order,
+                      window=args.window, **gate)
+
+    block = args.block_steps if args.block_steps > 0 else None
+    feeder = new_feeder()
+
     def one_step():
+        nonlocal feeder
         prog.reset()
         for k in phase:
             phase[k] = 0
-        return run_feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=on_step, order=args.order,
-                          window=args.window, **gate)
+        if block is None:                      # the whole batch, every bench step
+            feeder = new_feeder()
+        return feeder.advance(block)
 
     for i in range(args.warmup):
         t = time.perf_counter()
-        r = one_step()
+        n, tok = one_step()
         torch.cuda.synchronize()
-        log(f"[bench] warmup {i}: {r.n_steps} engine steps, {r.tokens} tokens, {time.perf_counter() - t:.2f} s")
+        log(f"[bench] warmup {i}: {n} engine steps, {tok} tokens, {time.perf_counter() - t:.2f} s")
+    first_timed = feeder.res.n_steps if block else 0
     eng.time_kernels(args.time_every, HBM_PEAK, MFMA_BF16_PEAK)
     torch.cuda.synchronize()
-    tokens = steps = prefill_tokens = 0
+    tokens = steps = prefill_tokens = decode_rows = 0
     t0 = time.perf_counter()
-    r = None
     for i in range(args.steps):
-        r = one_step()
-        tokens += r.tokens
-        steps += r.n_steps
+        t = time.perf_counter()
+        n, tok = one_step()
+        tokens += tok
+        steps += n
         prefill_tokens += phase["prefill_tokens"]
-        log(f"[bench] step {i}: {r.n_steps} engine steps ({phase['prefill_steps']} with prefill), "
-            f"{r.tokens} tokens, {phase['prefill_tokens']} prompt tokens prefilled")
+        decode_rows += phase["decode_rows"]
+        log(f"[bench] step {i}: {n} engine steps ({phase['prefill_steps']} with prefill), "
+            f"{tok} tokens, {phase['prefill_tokens']} prompt tokens prefilled, "
+            f"{phase['decode_rows'] / max(n, 1):.0f} decode rows per engine step, {time.perf_counter() - t:.2f} s (host)")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     config = {"workload": cfg.name, "models": len(mids), "queries": wl.n_queries,
-              "expert_calls": len(wl.max_new), "generated_tokens_per_step": tokens // args.steps,
-              "prefill_tokens_per_step": prefill_tokens // args.steps,
-              "engine_steps_per_step": steps // args.steps, "seed": args.seed,
-              "parallelism": "single GPU"}
-    extra = {"prefill_tokens_per_s": prefill_tokens / wall, "makespan_s": wall / args.steps}
+              "expert_calls": len(wl.max_new), "seed": args.seed, "parallelism": "single GPU",
+              "order": args.order}
+    if block:
+        config["slice"] = (f"engine steps {first_timed}..{first_timed + steps - 1} of the workload's "
+                           f"schedule (bench step = {block} engine steps; warm-up = steps 0..{first_timed - 1})")
+        config["block_steps"] = block
+        config["first_timed_engine_step"] = first_timed
+    else:
+        config["slice"] = "the whole batch per bench step"
+    config["engine_steps_timed"] = steps
+    config["generated_tokens_timed"] = tokens
+    config["prefill_tokens_timed"] = prefill_tokens
+    config["decode_rows_per_engine_step"] = round(decode_rows / max(steps, 1), 1)
+    extra = {"prefill_tokens_per_s": prefill_tokens / wall}
+    if block is None:
+        extra["makespan_s"] = wall / args.steps
     if cfg.aggregator:
-        extra["aggregation"] = {"aggregator_calls": r.agg_calls, "skipped_by_gate": len(r.gated),
+        r = feeder.res
+        extra["aggregation"] = {"aggregator_calls_submitted": r.agg_calls, "skipped_by_gate": len(r.gated),
                                 "gate_tau": args.gate_tau, "answer_options": args.answer_options if gate else None,
                                 "answer": "first generated token mod answer_options" if gate else None}
-    config["order"] = args.order
     if args.window is not None:
         config["window"] = args.window
     return tokens, wall, config, extra, wl
@@ -460,13 +577,14 @@ def schedule_study(args, cfg):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1)
-    ap.add_argument("--warmup", type=int, default=1)
-    ap.add_argument("--workload", default="moa-4x1b-bf16")
+    ap.add_argument("--steps", type=int, default=20, help="timed bench steps")
+    ap.add_argument("--warmup", type=int, default=5, help="untimed bench steps before them")
+    ap.add_argument("--workload", default="moa-3+1x8b-bf16")
+    ap.add_argument("--block-steps", type=int, default=128,
+                    help="engine steps per bench step (0: the whole batch per bench step)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--queries", type=int, default=None, help="fewer queries (quick runs only)")
     ap.add_argument("--time-every", type=int, default=8, help="time the kernels of 1 step in N")
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gate-tau", type=float, default=None,
                     help="adaptive-aggregation gate threshold (skip the aggregator when the experts' vote share >= tau)")
@@ -481,9 +599,11 @@ def main():
                          "priced by a per-step cost model (no GPU)")
     ap.add_argument("--window", type=int, default=None,
                     help="submission window of the feeder (default: every expert call up front)")
-    ap.add_argument("--one-stream", action="store_true",
-                    help="run every kernel on one stream (default: a several-model batch splits its "
-                         "models over two overlapping streams)")
+    ap.add_argument("--streams", type=int, default=None, choices=[1, 2],
+                    help="model streams of a several-model bf16 batch: 1 runs every kernel on the "
+                         "caller's stream, 2 splits each step's models over two overlapping streams "
+                         f"(default: {DEFAULT_STREAMS})")
+    ap.add_argument("--one-stream", action="store_true", help="same as --streams 1")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized device buffer 8 times (HBM counter calibration) and exit")
     args = ap.parse_args()
@@ -516,8 +636,9 @@ def main():
         return
     straggler = cfg.name.startswith("straggler")
     n_models = cfg.n_experts + (1 if cfg.aggregator else 0)
-    eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models, one_stream=args.one_stream)
-    streams = 1 if (args.one_stream or n_models < 2 or cfg.dtype != "bf16") else 2
+    want = 1 if args.one_stream else (args.streams or DEFAULT_STREAMS)
+    eng = Engine(cfg.model, cfg.dtype, cfg.engine, n_models, one_stream=want == 1)
+    streams = 1 if (want == 1 or n_models < 2 or cfg.dtype != "bf16") else 2
     log(f"[bench] {cfg.name}: {n_models} model(s); arena {eng.arena_bytes / 2**30:.1f} GiB")
     mids, weights0 = load_models(eng, cfg, args.seed, n_models)
     read_bps, mfma_fps = eng.measure_peaks()
@@ -531,9 +652,11 @@ def main():
         roof["overlap"] = ("launch durations from two model streams whose kernels run concurrently: "
                            "each launch carries half the batch's models and shares the GPU with the "
                            "other stream's launches (--one-stream times them alone)")
-    run_roof_ms = sum(s["roof_ms_all"] for s in stats.values())
+    from paper_2606_03014_amd.moa import VIEW_CLASSES
+    real = {k: v for k, v in stats.items() if k not in VIEW_CLASSES}
+    run_roof_ms = sum(s["roof_ms_all"] for s in real.values())
     # kernel time of every launch, estimated from the timed sample of each class
-    busy_ms = sum(s["ms"] / s["launches"] * s["launches_all"] for s in stats.values() if s["launches"])
+    busy_ms = sum(s["ms"] / s["launches"] * s["launches_all"] for s in real.values() if s["launches"])
 
     out = {
         "metric": METRIC,
@@ -543,6 +666,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": wall * 1e3 / args.steps,
+        "timed_wall_s": wall,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -550,6 +674,7 @@ def main():
         "data": "synthetic",
         "config": config,
         "roofline": roof,
+        "bars": design_bars(stats),
         "run_roofline": {"roof_ms": run_roof_ms / args.steps, "measured_ms": wall * 1e3 / args.steps,
                          "frac": run_roof_ms / (wall * 1e3),
                          "kernel_ms_est": busy_ms / args.steps, "gpu_busy_frac": busy_ms / (wall * 1e3)},
@@ -558,8 +683,8 @@ def main():
         # max(bytes / measured read bandwidth, useful flops / measured MFMA rate))
         "measured_peaks": {"hbm_read_GBps": read_bps / 1e9, "mfma_bf16_TFLOPs": mfma_fps / 1e12},
         "run_roofline_measured_peaks": {
-            "roof_ms": sum(max(s["bytes_all"] / read_bps, s["flops_all"] / mfma_fps) for s in stats.values()) * 1e3 / args.steps,
-            "frac": sum(max(s["bytes_all"] / read_bps, s["flops_all"] / mfma_fps) for s in stats.values()) / wall},
+            "roof_ms": sum(max(s["bytes_all"] / read_bps, s["flops_all"] / mfma_fps) for s in real.values()) * 1e3 / args.steps,
+            "frac": sum(max(s["bytes_all"] / read_bps, s["flops_all"] / mfma_fps) for s in real.values()) / wall},
     }
     out.update(extra)
     eng.close()
@@ -567,9 +692,9 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         if straggler:
-            out["cpu_baseline"] = cpu_baseline_history(cfg, args.seed, weights0, args.cpu_budget)
+            out["cpu_baseline"] = cpu_baseline_history(cfg, args.seed, weights0)
         else:
-            out["cpu_baseline"] = cpu_baseline(cfg, wl, weights0, args.cpu_budget)
+            out["cpu_baseline"] = cpu_baseline(cfg, wl, weights0)
     print(json.dumps(out), flush=True)
 
 

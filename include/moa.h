@@ -100,6 +100,8 @@ typedef struct {
   int32_t running;         /* running after the step */
   int32_t pending;         /* waiting for admission after the step */
   int32_t free_blocks;     /* free KV blocks after the step */
+  int32_t emitted;         /* tokens the step produces: its decode rows plus the
+                              requests whose prompt completes in it */
 } moa_step_info;
 
 typedef struct {
@@ -241,6 +243,12 @@ moa_status moa_debug_capture_logits(moa_engine* e, int64_t request_id, float* ho
 enum {
   MOA_K_EMBED = 0, MOA_K_NORM, MOA_K_GEMM_QKV, MOA_K_ROPE_KV, MOA_K_ATTN, MOA_K_ATTN_REDUCE,
   MOA_K_GEMM_O, MOA_K_GEMM_GATEUP, MOA_K_GEMM_DOWN, MOA_K_GEMM_LMHEAD, MOA_K_ARGMAX, MOA_K_PREFILL_ATTN,
+  /* Two views of the GEMM launches above, by the kernel that runs them: every
+   * qkv / o / gate-up / down / LM-head launch is counted once more in exactly
+   * one of these (the workgroup-tile kernel of small and medium row counts,
+   * or the 128-row-tile matrix-core kernel of large row counts). A sum over
+   * classes must leave them out. */
+  MOA_K_GEMM_SMALL_M, MOA_K_GEMM_LARGE_M,
   MOA_K_COUNT
 };
 

@@ -5,6 +5,6 @@ C++ host engine behind the C ABI of include/moa.h); this package is its thin
 Python binding (``moa``) and the host feeder (``engine``).
 """
 from . import moa
-from .engine import Engine, run_feeder, run_straggler, engine_cfg, model_cfg
+from .engine import Engine, Feeder, run_feeder, run_straggler, engine_cfg, model_cfg
 
-__all__ = ["moa", "Engine", "run_feeder", "run_straggler", "engine_cfg", "model_cfg"]
+__all__ = ["moa", "Engine", "Feeder", "run_feeder", "run_straggler", "engine_cfg", "model_cfg"]

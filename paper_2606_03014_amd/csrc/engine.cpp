@@ -246,7 +246,7 @@ struct moa_engine {
   size_t pinned_out_cap = 0;
 
   // kernel timing (inspection hook): event pairs around launches of sampled steps
-  struct Timed { int cls; hipEvent_t a, b; double bytes, flops; };
+  struct Timed { int cls, cls2; hipEvent_t a, b; double bytes, flops; };
   int time_every = 0;
   bool time_now = false;
   bool account = false;
@@ -307,11 +307,14 @@ moa_status resolve_timed(moa_engine* e) {
       e->ev_pool.push_back(t.b);
       continue;
     }
-    moa_kernel_stats& k = e->kstats[t.cls];
-    k.launches += 1;
-    k.ms += ms;
-    k.bytes += t.bytes;
-    k.flops += t.flops;
+    for (int c : {t.cls, t.cls2}) {
+      if (c < 0) continue;
+      moa_kernel_stats& k = e->kstats[c];
+      k.launches += 1;
+      k.ms += ms;
+      k.bytes += t.bytes;
+      k.flops += t.flops;
+    }
     e->ev_pool.push_back(t.a);
     e->ev_pool.push_back(t.b);
   }
@@ -320,17 +323,21 @@ moa_status resolve_timed(moa_engine* e) {
 }
 
 // Launch `call` (an expression yielding hipError_t). Every launch is
-// accounted (algorithmic bytes, flops, roofline time); in sampled steps the
+// accounted (algorithmic bytes, flops, roofline time) under class `cls` and,
+// when cls2 >= 0, under the view class cls2 too; in sampled steps the
 // kernel's own dispatch also carries a start/stop event pair.
-#define LAUNCH(cls, bytes_, flops_, call, what)                                   \
+#define LAUNCH2(cls, cls2, bytes_, flops_, call, what)                            \
   do {                                                                           \
     if (e->account) {                                                            \
-      moa_kernel_stats& _k = e->kstats[(cls)];                                   \
       const double _by = (double)(bytes_), _fl = (double)(flops_);               \
-      _k.launches_all += 1;                                                      \
-      _k.bytes_all += _by;                                                       \
-      _k.flops_all += _fl;                                                       \
-      _k.roof_ms_all += 1e3 * std::max(_by / e->peak_bw, _fl / e->peak_flops);   \
+      for (int _c : {(int)(cls), (int)(cls2)}) {                                 \
+        if (_c < 0) continue;                                                    \
+        moa_kernel_stats& _k = e->kstats[_c];                                    \
+        _k.launches_all += 1;                                                    \
+        _k.bytes_all += _by;                                                     \
+        _k.flops_all += _fl;                                                     \
+        _k.roof_ms_all += 1e3 * std::max(_by / e->peak_bw, _fl / e->peak_flops); \
+      }                                                                          \
     }                                                                            \
     if (e->time_now) {                                                           \
       hipEvent_t _a = pool_event(e), _b = pool_event(e);                         \
@@ -339,11 +346,15 @@ moa_status resolve_timed(moa_engine* e) {
       hipError_t _err = (call);                                                  \
       set_launch_events(nullptr, nullptr);                                       \
       if (_err != hipSuccess) return hip_fail(e, _err, what);                    \
-      e->timed.push_back({(cls), _a, _b, (double)(bytes_), (double)(flops_)});  \
+      e->timed.push_back({(cls), (cls2), _a, _b, (double)(bytes_), (double)(flops_)}); \
     } else {                                                                     \
       HIPCHK((call), what);                                                      \
     }                                                                            \
   } while (0)
+#define LAUNCH(cls, bytes_, flops_, call, what) LAUNCH2(cls, -1, bytes_, flops_, call, what)
+// a GEMM launch: its projection class plus the view of the kernel that runs it
+#define LAUNCH_GEMM(cls, mt_, bytes_, flops_, call, what) \
+  LAUNCH2(cls, (mt_) == kBigTile ? MOA_K_GEMM_LARGE_M : MOA_K_GEMM_SMALL_M, bytes_, flops_, call, what)
 
 // Tile-shuffle a row-major [N][K] bf16 matrix into MFMA B-fragment order:
 // fragment (n/16, k/32) is 64 lanes x 8 contiguous elements, lane = n%16 +
@@ -1025,7 +1036,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wqkv[l]; }), b.g0, b.ng, d, qkv, EPI_F32, e->xn,
                   xn_lo, b.part, nullptr, 0, true, ga, mt, nt);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH(MOA_K_GEMM_QKV, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "qkv gemm");
+        LAUNCH_GEMM(MOA_K_GEMM_QKV, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "qkv gemm");
         LAUNCH(MOA_K_ROPE_KV, (double)b.nr * qkv * 4.0 * ga.S + (double)b.nr * (nh * hd * 4.0 + 2.0 * nkv * hd * esz), 0,
                launch_rope_kv(st, bf, b.part + ro * qkv, ga.S, ga.out_split, sd.row_pos + ro, sd.row_bt + ro,
                               e->bt_store, e->rope, e->q + ro * nh * hd, e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd,
@@ -1046,7 +1057,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), b.g0, b.ng, nh * hd, d, EPI_F32, e->ao,
                   ao_lo, b.part, nullptr, 0, true, ga, mt, nt);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH(MOA_K_GEMM_O, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "o gemm");
+        LAUNCH_GEMM(MOA_K_GEMM_O, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "o gemm");
         LAUNCH(MOA_K_NORM, norm_bytes + ga.S * (double)b.nr * d * 4.0, 0,
                launch_add_rmsnorm(st, bf, e->x + ro * d, b.part + ro * d, ga.S, ga.out_split, nullptr,
                                   sd.row_model + ro, b.nr, fill([l](const ModelDev& x) { return x.mlp_norm[l]; }),
@@ -1055,18 +1066,18 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
           plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), b.g0, b.ng, d, 2 * F, EPI_SWIGLU,
                     e->xn, xn_lo, nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt);
           gemm_cost(ga, EPI_SWIGLU, gb, gf);
-          LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(st, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
+          LAUNCH_GEMM(MOA_K_GEMM_GATEUP, mt, gb, gf, launch_gemm(st, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
         } else {
           plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), b.g0, b.ng, d, 2 * F, EPI_F32, e->xn, 0,
                     b.part, nullptr, 0, false, ga, mt, nt);
           gemm_cost(ga, EPI_F32, gb, gf);
-          LAUNCH(MOA_K_GEMM_GATEUP, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
+          LAUNCH_GEMM(MOA_K_GEMM_GATEUP, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
           HIPCHK(launch_swiglu_f32(st, b.part + ro * 2 * F, (float*)e->h + ro * F, b.nr, F), "swiglu");
         }
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wdown[l]; }), b.g0, b.ng, F, d, EPI_F32, e->h, h_lo,
                   b.part, nullptr, 0, true, ga, mt, nt);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH(MOA_K_GEMM_DOWN, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "down gemm");
+        LAUNCH_GEMM(MOA_K_GEMM_DOWN, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "down gemm");
         b.prev_split = ga.S;
         b.prev_stride = ga.out_split;
       }
@@ -1103,7 +1114,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
         int mt, nt;
         plan_gemm(e, lin, lg0, lng, d, V, EPI_F32, e->xl, xl_lo, e->logits, nullptr, 0, false, ga, mt, nt);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH(MOA_K_GEMM_LMHEAD, gb, gf, launch_gemm(b.st, bf, ga, EPI_F32, mt, nt), "lm head");
+        LAUNCH_GEMM(MOA_K_GEMM_LMHEAD, mt, gb, gf, launch_gemm(b.st, bf, ga, EPI_F32, mt, nt), "lm head");
         LAUNCH(MOA_K_ARGMAX, (double)nb * V * 4.0, 0,
                launch_argmax(b.st, e->logits + (size_t)b0 * V, nb, V, sd.lm_dst + b0, e->tok_store), "argmax");
       }
@@ -1385,6 +1396,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
     info->running = (int32_t)e->running.size();
     info->pending = (int32_t)e->pending.size();
     info->free_blocks = (int32_t)e->free_blocks.nfree;
+    info->emitted = R;
   }
   return MOA_OK;
 }

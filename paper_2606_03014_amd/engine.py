@@ -145,9 +145,9 @@ def expert_order(workload, order):
     raise ValueError(order)
 
 
-def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None,
-               gate_tau=None, answer_of=None, order="first-seen", window=None):
-    """Drive ``eng`` through ``workload`` (a moa_inputs.Workload).
+class Feeder:
+    """The host feeder of one workload, resumable: ``advance(n)`` runs at most
+    n engine steps, so a caller can time a fixed window of the schedule.
 
     expert_models[e] is the engine model id of expert e; agg_model is the
     aggregator's model id (-1: none). A workload without experts sends every
@@ -165,88 +165,113 @@ def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_ste
     submitted as admissions make room, while aggregator calls are submitted
     the moment their experts finish, so they overtake the expert calls not
     yet submitted (aggregation fills the gaps of the expert tail instead of
-    queueing behind every expert call)."""
-    res = FeedResult()
-    who = {}
-    tau = None if gate_tau is None else Fraction(gate_tau).limit_denominator(64)
-    if window is not None and window < 1:
-        raise ValueError("window must be >= 1")
-    queue = list(expert_order(workload, order))
-    nxt = 0
-    submitted = admitted = 0
+    queueing behind every expert call).
 
-    def top_up():
-        nonlocal nxt, submitted
+    Each engine step collects what retired one step earlier, so the schedule
+    (and when aggregator calls are submitted) is a function of step indices
+    only, whatever the caller's step windows are."""
+
+    def __init__(self, eng, workload, expert_models, agg_model=-1, on_step=None, gate_tau=None,
+                 answer_of=None, order="first-seen", window=None):
+        if window is not None and window < 1:
+            raise ValueError("window must be >= 1")
+        self.eng, self.wl, self.experts, self.agg = eng, workload, list(expert_models), agg_model
+        self.on_step = on_step
+        self.answer_of = answer_of
+        self.tau = None if gate_tau is None else Fraction(gate_tau).limit_denominator(64)
+        self.window = window
+        self.res = FeedResult()
+        self.who = {}
+        self.queue = list(expert_order(workload, order))
+        self.nxt = 0
+        self.submitted = self.admitted = 0
+        self.last = -1
+        self.emitted = 0         # tokens produced by the engine steps run so far
+        self.done = False
+        self._top_up()
+        self.remaining = ({q: len(ex) for q, ex in enumerate(workload.experts) if ex}
+                          if agg_model >= 0 else {})
+        if agg_model >= 0 and workload.n_experts == 0:
+            for q in range(workload.n_queries):
+                self._submit(q, workload.prompts[q], agg_model, -1, workload.agg_max_new)
+                self.res.agg_calls += 1
+
+    def _submit(self, q, tokens, model, e, G):
+        rid = self.eng.submit(tokens, model, G)
+        self.res.rid_of[(q, model)] = rid
+        self.who[rid] = (q, model, e)
+        self.submitted += 1
+
+    def _top_up(self):
         n = 0
-        while nxt < len(queue) and (window is None or submitted - admitted < window):
-            q, e, G = queue[nxt]
-            nxt += 1
-            rid = eng.submit(workload.prompts[q], expert_models[e], G)
-            res.rid_of[(q, expert_models[e])] = rid
-            who[rid] = (q, expert_models[e], e)
-            submitted += 1
+        while self.nxt < len(self.queue) and (self.window is None or
+                                              self.submitted - self.admitted < self.window):
+            q, e, G = self.queue[self.nxt]
+            self.nxt += 1
+            self._submit(q, self.wl.prompts[q], self.experts[e], e, G)
             n += 1
         return n
 
-    top_up()
-    remaining = {q: len(ex) for q, ex in enumerate(workload.experts) if ex} if agg_model >= 0 else {}
-    if agg_model >= 0 and workload.n_experts == 0:
-        for q in range(workload.n_queries):
-            rid = eng.submit(workload.prompts[q], agg_model, workload.agg_max_new)
-            res.rid_of[(q, agg_model)] = rid
-            who[rid] = (q, agg_model, -1)
-            res.agg_calls += 1
-            submitted += 1
-
-    def handle(done, after):
-        nonlocal submitted
+    def _handle(self, done, after):
+        res, wl = self.res, self.wl
         if done:
             res.collects.append((after, [d[0] for d in done]))
         ready = []
         for rid, mdl, fin, toks in done:
-            q, m, e = who[rid]
+            q, m, e = self.who[rid]
             res.outputs[(q, m)] = toks
             res.tokens += len(toks)
-            if q in remaining and e >= 0:
-                remaining[q] -= 1
-                if remaining[q] == 0:
+            if q in self.remaining and e >= 0:
+                self.remaining[q] -= 1
+                if self.remaining[q] == 0:
                     ready.append(q)
         for q in sorted(ready):
-            del remaining[q]
-            if tau is not None:
-                conf, majority = plurality([answer_of(q, e, res.outputs[(q, expert_models[e])])
-                                            for e in workload.experts[q]])
-                if conf >= tau:
+            del self.remaining[q]
+            if self.tau is not None:
+                conf, majority = plurality([self.answer_of(q, e, res.outputs[(q, self.experts[e])])
+                                            for e in wl.experts[q]])
+                if conf >= self.tau:
                     res.gated[q] = majority
                     continue
-            parts = [workload.prompts[q]] + [res.outputs[(q, expert_models[e])] for e in workload.experts[q]]
-            rid = eng.submit(np.concatenate(parts).astype(np.int32), agg_model, workload.agg_max_new)
-            res.rid_of[(q, agg_model)] = rid
-            who[rid] = (q, agg_model, -1)
+            parts = [wl.prompts[q]] + [res.outputs[(q, self.experts[e])] for e in wl.experts[q]]
+            self._submit(q, np.concatenate(parts).astype(np.int32), self.agg, -1, wl.agg_max_new)
             res.agg_calls += 1
-            submitted += 1
         return len(ready)
 
-    last = -1
-    while True:
-        info = eng.step()
-        if info.step < 0:
-            n = handle(eng.collect(last), last)
-            m = top_up()
-            if n == 0 and m == 0:
-                break
-            continue
-        last = info.step
-        admitted += info.admitted
-        res.n_steps += 1
-        if on_step is not None:
-            on_step(info)
-        if last >= 1:
-            handle(eng.collect(last - 1), last - 1)
-        top_up()
-        if max_steps is not None and res.n_steps >= max_steps:
-            break
-    return res
+    def advance(self, max_steps=None):
+        """Run engine steps until the workload is done or max_steps steps ran;
+        returns (engine steps run, tokens those steps produced)."""
+        steps = tokens = 0
+        eng = self.eng
+        while not self.done and (max_steps is None or steps < max_steps):
+            info = eng.step()
+            if info.step < 0:
+                n = self._handle(eng.collect(self.last), self.last)
+                m = self._top_up()
+                if n == 0 and m == 0:
+                    self.done = True
+                continue
+            self.last = info.step
+            self.admitted += info.admitted
+            self.res.n_steps += 1
+            steps += 1
+            tokens += info.emitted
+            if self.on_step is not None:
+                self.on_step(info)
+            if self.last >= 1:
+                self._handle(eng.collect(self.last - 1), self.last - 1)
+            self._top_up()
+        self.emitted += tokens
+        return steps, tokens
+
+
+def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None,
+               gate_tau=None, answer_of=None, order="first-seen", window=None):
+    """Drive ``eng`` through ``workload`` (a moa_inputs.Workload) to the end,
+    or for at most max_steps engine steps; see Feeder for the arguments."""
+    f = Feeder(eng, workload, expert_models, agg_model, on_step, gate_tau, answer_of, order, window)
+    f.advance(max_steps)
+    return f.res
 
 
 def run_straggler(eng, sw, model_id=0, host_kv_fn=None, on_step=None, after_collect=False):

@@ -35,7 +35,7 @@ class moa_engine_cfg(C.Structure):
 class moa_step_info(C.Structure):
     _fields_ = [("step", C.c_int64), ("admitted", C.c_int32), ("prefill_tokens", C.c_int32),
                 ("decode_rows", C.c_int32), ("finished", C.c_int32), ("running", C.c_int32),
-                ("pending", C.c_int32), ("free_blocks", C.c_int32)]
+                ("pending", C.c_int32), ("free_blocks", C.c_int32), ("emitted", C.c_int32)]
 
 
 class moa_result(C.Structure):
@@ -56,7 +56,10 @@ class moa_kernel_stats(C.Structure):
 
 
 KERNEL_CLASSES = ["embed", "norm", "gemm_qkv", "rope_kv", "attn", "attn_reduce", "gemm_o",
-                  "gemm_gateup", "gemm_down", "gemm_lmhead", "argmax", "prefill_attn"]
+                  "gemm_gateup", "gemm_down", "gemm_lmhead", "argmax", "prefill_attn",
+                  "gemm_small_m", "gemm_large_m"]
+# views: every GEMM launch is counted again in one of these (leave them out of sums over classes)
+VIEW_CLASSES = ("gemm_small_m", "gemm_large_m")
 
 P = C.POINTER
 _SIGS = {

@@ -54,6 +54,42 @@ def test_binding_constants_match_the_header():
     assert consts["MOA_FLAG_PLAN_ONLY"] & consts["MOA_FLAG_ONE_STREAM"] == 0
 
 
+def test_kernel_classes_follow_the_header_enum():
+    """The binding's kernel-class names index moa_debug_kernel_stats' array in
+    the order of the header's MOA_K_* enum, and the two GEMM views are last."""
+    hdr = open(os.path.join(ROOT, "include", "moa.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    body = hdr[hdr.index("MOA_K_EMBED = 0"):hdr.index("MOA_K_COUNT")]
+    names = [n.lower() for n in re.findall(r"MOA_K_([A-Z_]+)", body)]
+    assert [n.replace("_", "") for n in names] == [c.replace("_", "") for c in M.KERNEL_CLASSES]
+    assert M.KERNEL_CLASSES[-2:] == list(M.VIEW_CLASSES)
+
+
+def test_feeder_in_blocks_matches_one_run_and_counts_every_token():
+    """Advancing the feeder a fixed number of engine steps at a time (the
+    benchmark's timed blocks) gives the same schedule as one uninterrupted
+    run, and the steps' emitted counts add up to every generated token."""
+    from paper_2606_03014_amd import Feeder
+    c = CONFIGS["moa-3+1x8b-bf16"]
+    wl = make_workload(c.name, 0, n_queries=48)
+    runs = []
+    for block in (None, 7, 128):
+        eng = _dry(c.model, c.engine, 4)
+        f = Feeder(eng, wl, [0, 1, 2], agg_model=3)
+        per_block = []
+        while not f.done:
+            per_block.append(f.advance(block))
+        steps = eng.steps()
+        eng.close()
+        assert sum(n for n, _ in per_block) == f.res.n_steps == len(steps)
+        if block is not None:
+            assert all(n == block for n, _ in per_block[:-2])
+        assert f.emitted == sum(t for _, t in per_block) == f.res.tokens
+        assert f.res.tokens == wl.total_expert_tokens() + f.res.agg_calls * wl.agg_max_new
+        runs.append((steps.tolist(), sorted(f.res.rid_of.items()), f.res.collects))
+    assert runs[0] == runs[1] == runs[2]
+
+
 def test_second_model_stream_reserves_one_partial_buffer():
     """A bf16 engine reserves split-K partials for its second model stream in
     the arena; MOA_FLAG_ONE_STREAM drops exactly that buffer, and fp32
