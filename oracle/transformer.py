@@ -28,7 +28,8 @@ bf16: k (after RoPE) and v are rounded to bf16 (nearest-even) when they are
 written to the cache, exactly once; everything else stays float64.
 
 Parity pins (tests/test_oracle_*.py): single-key attention returns V, equal
-keys average V, softmax rows sum to 1, RoPE is the identity at position 0 and
+keys average V, softmax rows sum to 1, the blockwise causal attention of a
+chunk equals attend() position by position, RoPE is the identity at position 0 and
 norm-preserving with relative-position scores, paged == contiguous KV bit for
 bit, cached decode == brute-force prefix recompute, the zero-layer model
 equals the closed form Wlm . n(E[t]), and a torch float64 functional model
@@ -97,6 +98,32 @@ def attend(q, K, V):
         s = K[:, kv, :] @ q[h] / np.sqrt(hd)
         p = softmax(s)
         out[h] = p @ V[:, kv, :]
+    return out
+
+
+def causal_attention(q, K, V, start, block=512):
+    """Causal attention of a chunk of query positions, all heads at once.
+
+    q: [T, n_h, hd] at positions start .. start + T - 1; K, V: the cache,
+    [start + T, n_kv, hd]. Row t attends to keys 0 .. start + t (the same
+    masked softmax(q . k / sqrt(hd)) . v as attend(), which defines it;
+    evaluated one block of query rows and one head at a time, so long
+    prompts cost a few library matmuls instead of a Python loop per
+    position). Returns [T, n_h, hd]."""
+    T, n_h, hd = q.shape
+    n_kv = K.shape[1]
+    group = n_h // n_kv
+    out = np.empty_like(q)
+    for b0 in range(0, T, block):
+        b1 = min(T, b0 + block)
+        kmax = start + b1                                    # keys this block can see
+        pos = start + np.arange(b0, b1)                      # query positions
+        future = np.arange(kmax)[None, :] > pos[:, None]     # key index past the query's position
+        for h in range(n_h):
+            kv = h // group
+            s = q[b0:b1, h, :] @ K[:kmax, kv, :].T / np.sqrt(hd)
+            s[future] = -np.inf
+            out[b0:b1, h, :] = softmax(s) @ V[:kmax, kv, :]
     return out
 
 
@@ -202,10 +229,7 @@ def forward_chunk(model, tokens, start, kv, bf16_kv=False, want="all"):
         v = store(v)
         kv.write(l, start, k, v)
         K, V = kv.read(l, start + T)
-        att = np.empty((T, n_h, hd))
-        for t in range(T):
-            att[t] = attend(q[t], K[: start + t + 1], V[: start + t + 1])
-        att = att.reshape(T, n_h * hd)
+        att = causal_attention(q, K, V, start).reshape(T, n_h * hd)
         h = x + att @ model.W(p + "wo").T
         hn = rmsnorm(h, model.W(p + "mlp_norm"), m.rms_eps)
         g = hn @ model.W(p + "w_gate").T

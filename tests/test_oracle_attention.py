@@ -56,6 +56,33 @@ def test_attend_matches_torch_sdpa_gqa(n_h, n_kv):
     np.testing.assert_allclose(T.attend(q, K, V), ref, rtol=0, atol=1e-13)
 
 
+@pytest.mark.parametrize("start,T_,n_h,n_kv,block", [(0, 1, 4, 4, 512), (0, 37, 8, 2, 512),
+                                                     (11, 37, 8, 2, 5), (300, 9, 32, 8, 4)])
+def test_causal_attention_equals_attend_per_position(start, T_, n_h, n_kv, block):
+    """The chunk attention of forward_chunk: row t against keys
+    0..start+t, exactly attend() on that prefix (blocks of query rows and a
+    chunk starting mid-sequence included)."""
+    r = _rng(40 + start + T_)
+    hd = 16
+    q = r.standard_normal((T_, n_h, hd)) * 3
+    K = r.standard_normal((start + T_, n_kv, hd))
+    V = r.standard_normal((start + T_, n_kv, hd))
+    got = T.causal_attention(q, K, V, start, block=block)
+    for t in range(T_):
+        np.testing.assert_allclose(got[t], T.attend(q[t], K[: start + t + 1], V[: start + t + 1]),
+                                   rtol=0, atol=1e-13)
+
+
+def test_causal_attention_first_position_returns_v():
+    r = _rng(41)
+    q = r.standard_normal((1, 8, 16))
+    K = r.standard_normal((1, 2, 16))
+    V = r.standard_normal((1, 2, 16))
+    out = T.causal_attention(q, K, V, 0)
+    for h in range(8):
+        assert np.array_equal(out[0, h], V[0, h // 4])
+
+
 def test_rope_identity_at_position_zero():
     r = _rng(5)
     x = r.standard_normal((1, 3, 64))

@@ -131,9 +131,25 @@ def test_bf16_kv_rounds_only_the_cache():
     err = np.abs(a - b).max()
     assert 0 < err < 5e-2 * np.abs(a).max()
     np.testing.assert_allclose(a, torch_logits(shape, w, toks), rtol=1e-10, atol=1e-12)
+    # the rounding points themselves: torch's own bf16 cast of k after RoPE
+    # and of v (never q), at the exact same places
+    np.testing.assert_allclose(b, torch_logits(shape, w, toks, bf16_kv=True), rtol=0, atol=1e-12)
     w2 = dict(w)
     for l in range(shape.n_layers):       # zero K/V projections: stored values are exact zeros
         w2[f"layers.{l}.wk"] = np.zeros_like(w[f"layers.{l}.wk"])
         w2[f"layers.{l}.wv"] = np.zeros_like(w[f"layers.{l}.wv"])
     om2 = T.OracleModel(shape, w2)
     assert np.array_equal(T.forward_full(om2, toks), T.forward_full(om2, toks, bf16_kv=True))
+
+
+@pytest.mark.parametrize("scale", [1.0, 25.0])
+def test_bf16_kv_cache_matches_torch_bfloat16_cache(scale):
+    """The bf16 K/V reading, pinned against torch: an independent decoder whose
+    cache holds torch.bfloat16(float32(k after RoPE)) and the same of v gives
+    the oracle's bf16_kv logits to 1e-12 (rounding k before RoPE, rounding q,
+    or skipping the float32 step each move them by far more)."""
+    om, w = _model(scale=scale, seed=4)
+    toks = _tokens(33, MINI.vocab, 9)
+    got = T.forward_full(om, toks, bf16_kv=True)
+    np.testing.assert_allclose(got, torch_logits(MINI, w, toks, bf16_kv=True), rtol=0, atol=1e-12)
+    assert np.abs(got - torch_logits(MINI, w, toks)).max() > 1e-6     # the rounding is really there

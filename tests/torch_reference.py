@@ -5,7 +5,8 @@ Used only to pin the oracle: attention is torch's scaled_dot_product_attention
 torch.nn.functional.silu, and RoPE is written as a complex rotation
 (pairs (i, i + hd/2) viewed as one complex number multiplied by
 exp(1j * pos * theta^(-2i/hd))), a different formulation from the oracle's
-real-valued rotate-half.
+real-valued rotate-half. With bf16_kv the cache values go through
+torch.bfloat16 (via float32), torch's own rounding.
 """
 import numpy as np
 import torch
@@ -29,7 +30,14 @@ def _rope_complex(x, pos, theta):
     return torch.cat([z.real, z.imag], dim=-1)
 
 
-def torch_logits(shape, weights, tokens, n_layers=None):
+def _bf16(x):
+    """Round to bf16 through float32, both nearest-even, back to float64."""
+    return x.to(torch.float32).to(torch.bfloat16).to(torch.float64)
+
+
+def torch_logits(shape, weights, tokens, n_layers=None, bf16_kv=False):
+    """Logits at every position. bf16_kv: the K/V cache holds bf16 values --
+    k after RoPE and v are rounded to bf16 once, q never."""
     L = shape.n_layers if n_layers is None else n_layers
     d, nh, nkv, hd = shape.d_model, shape.n_heads, shape.n_kv_heads, shape.head_dim
     eps = shape.rms_eps
@@ -45,6 +53,8 @@ def torch_logits(shape, weights, tokens, n_layers=None):
         v = (xn @ W("wv").T).view(T, nkv, hd).transpose(0, 1)
         q = _rope_complex(q, pos, shape.rope_theta)
         k = _rope_complex(k, pos, shape.rope_theta)
+        if bf16_kv:
+            k, v = _bf16(k), _bf16(v)
         a = F.scaled_dot_product_attention(q[None], k[None], v[None], is_causal=True,
                                            enable_gqa=True)[0]
         h = x + a.transpose(0, 1).reshape(T, nh * hd) @ W("wo").T
