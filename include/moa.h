@@ -234,10 +234,11 @@ moa_status moa_debug_step_shares(moa_engine* e, int32_t* n_shares, int32_t* n_mo
 
 /* Capture the fp32 logits row of every token request_id emits: row j (the
  * logits that produced output token j) is copied to host_logits + j * vocab
- * once the step that computes it completes. host_logits must hold
- * max_new_tokens * vocab floats and stay valid until the request is
- * collected. Must be registered before the request's prefill completes. */
-moa_status moa_debug_capture_logits(moa_engine* e, int64_t request_id, float* host_logits);
+ * once the step that computes it completes. cap: floats host_logits holds;
+ * EINVAL (nothing registered) when it is below max_new_tokens * vocab. The
+ * buffer must stay valid until the request is collected. ESTATE when the
+ * request's prefill has already completed (register before it). */
+moa_status moa_debug_capture_logits(moa_engine* e, int64_t request_id, float* host_logits, int64_t cap);
 
 /* Kernel classes of one step (for moa_debug_time_kernels). */
 enum {

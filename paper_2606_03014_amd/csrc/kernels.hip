@@ -250,123 +250,19 @@ __global__ __launch_bounds__(1024) void k_add_rmsnorm(float* __restrict__ x, con
   }
 }
 
-// ------------------------------------------------------------ bf16 GEMM
-// Y = X . W^T for every group (model) of rows, on MFMA 16x16x32 bf16.
+// ------------------------------------------------------------ bf16 GEMMs
+// Y = X . W^T for every group (model) of rows, on bf16 MFMA with fp32
+// accumulation; X arrives as a split-bf16 pair (hi + lo planes), so each
+// weight fragment meets two MFMAs.
 //
-// Work unit = one wavefront: a chunk of 16*MT rows x NT tiles of 16 output
-// columns x one k-split. Weights are stored tile-shuffled so that one MFMA
-// B-fragment (16 columns x 32 k) is 1 KB contiguous, lane-ordered: a wave's
-// weight read is a single fully coalesced 1 KB burst per fragment, and a
-// 16-column tile streams K*32 bytes contiguously. Waves of one workgroup
-// cover consecutive row chunks of the same columns, so a weight fragment
-// reaches HBM once and the other waves hit the cache.
+// Weights are stored tile-shuffled so that one MFMA B-fragment (16 columns x
+// 32 k) is 1 KB contiguous, lane-ordered: a wave's weight read is a single
+// fully coalesced 1 KB burst per fragment, and a 16-column tile streams
+// K*32 bytes contiguously.
 //
-// MFMA operand layout used here (lane l of 64): A = rows l%16, k = 8*(l/16)..+8;
+// 16x16x32 operand layout (lane l of 64): A = rows l%16, k = 8*(l/16)..+8;
 // B = column l%16, same k; D = column l%16, rows 4*(l/16)..+4.
-template <int MT, int NT, int EPI, int U>
-__global__ __launch_bounds__(256) void k_gemm_bf16(GemmArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (item >= a.total_items) return;
-  const void* Wg = a.g[0].W;
-  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
-#pragma unroll
-  for (int i = 1; i < kMaxGroups; ++i) {
-    if (i < a.ngroups && a.g[i].item0 <= item) {
-      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
-    }
-  }
-  const int idx = item - item0;
-  const int mc = idx % n_mc;
-  const int rest = idx / n_mc;
-  const int s = rest % a.S;
-  const int nb = rest / a.S;
-  const int ks0 = s * a.ksteps;
-  const int nt0 = nb * NT;
-  const int KS = a.K >> 5;
-
-  const uint4* W = (const uint4*)Wg;
-  const uint4* wp[NT];
-#pragma unroll
-  for (int j = 0; j < NT; ++j) wp[j] = W + ((size_t)(nt0 + j) * KS + ks0) * 64 + lane;
-
-  const int rbase = row0 + mc * MT * 16;
-  const int rend = row0 + nrows;
-  const uint16_t* X = (const uint16_t*)a.X;
-  const uint4* xp[MT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m) {
-    int r = min(rbase + m * 16 + (lane & 15), rend - 1);
-    xp[m] = (const uint4*)(X + (size_t)r * a.K + ks0 * 32 + (lane >> 4) * 8);
-  }
-  const size_t xlo = a.x_lo / 8;     // hi -> lo plane distance in uint4 units
-
-  f32x4_t acc[MT][NT];
-#pragma unroll
-  for (int m = 0; m < MT; ++m)
-#pragma unroll
-    for (int j = 0; j < NT; ++j) acc[m][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  for (int kk = 0; kk < a.ksteps; kk += U) {
-    uint4 b[U][NT], xa[U][MT], xl[U][MT];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int j = 0; j < NT; ++j) b[u][j] = wp[j][(kk + u) * 64];
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int m = 0; m < MT; ++m) {
-        xa[u][m] = xp[m][(kk + u) * 4];
-        xl[u][m] = xp[m][(kk + u) * 4 + xlo];
-      }
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xa[u][m]),
-                                                              __builtin_bit_cast(bf16x8_t, b[u][j]),
-                                                              acc[m][j], 0, 0, 0);
-          acc[m][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xl[u][m]),
-                                                              __builtin_bit_cast(bf16x8_t, b[u][j]),
-                                                              acc[m][j], 0, 0, 0);
-        }
-  }
-
-  const int col = lane & 15;
-  const int rq = (lane >> 4) * 4;
-  if (EPI == EPI_F32) {
-    float* out = a.out + (size_t)s * a.out_split;
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = rbase + m * 16 + rq + i;
-          if (r < rend) out[(size_t)r * a.N + (nt0 + j) * 16 + col] = acc[m][j][i];
-        }
-  } else {
-    // tiles (2p, 2p+1) are (gate, up) of the same 16 hidden units
-    const int half = a.N >> 1;
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-      for (int p = 0; p < NT / 2; ++p)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int r = rbase + m * 16 + rq + i;
-          if (r < rend) {
-            const float g = acc[m][2 * p][i], u = acc[m][2 * p + 1][i];
-            const float hv = g / (1.f + __expf(-g)) * u;
-            store_split(a.hout, a.h_lo, (size_t)r * half + ((nt0 >> 1) + p) * 16 + col, hv);
-          }
-        }
-  }
-}
-
+//
 // --------------------------------------- bf16 GEMM, workgroup-tile variant
 // A workgroup (4 wavefronts) owns 16*MT rows x 64*NT columns x one k-split.
 // Per stage of 4 MFMA k-steps (128 k) the split-bf16 activation block (both
@@ -726,6 +622,185 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) 
           }
         }
       }
+  }
+}
+
+// ------------------------------------------- medium-M GEMM (16x16x32 MFMA)
+// Decode batches put a few dozen to a few hundred rows on each model, so
+// every weight byte feeds only that many rows of MFMA work: the GEMM must
+// stream the weights at HBM speed. A workgroup of 4 waves owns up to 16*RT
+// rows of one model (all of them, for groups up to that size, so each weight
+// tile leaves HBM once per step) x 4 * CT * 16 columns x one k-split.
+//  * The split-bf16 activation block of a 32-k stage (2*RT fragments of 1 KB,
+//    both planes) is shared by the four waves: it goes HBM/L2 -> LDS by
+//    direct loads into a ring of D + 1 slots.
+//  * Each wave streams its own CT weight tiles (1 KB fragments) straight into
+//    a register ring D stages deep, so the LDS holds only activations and two
+//    workgroups fit on a CU: the planner keeps the whole grid resident at once
+//    (a grid of more items than slots ran at half the streaming rate in its
+//    last, partly empty round).
+//  * Per stage a wave multiplies the hi plane while the lo plane's fragments
+//    are read; the RT x CT accumulators form that many independent MFMA
+//    chains (16x16x32 needs about 16 to reach its rate).
+//  * Loads complete in issue order: stage s's activation loads, then its
+//    weight loads, so waiting until D - 1 stages' worth of loads are
+//    outstanding makes stage s resident.
+//  * k-splits take KS / S k-steps each, rounded (any S).
+__device__ __forceinline__ u32x4 ds_read_b128(unsigned addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+  return v;
+}
+__device__ __forceinline__ void tie(u32x4& v) { asm volatile("" : "+v"(v)); }
+
+template <int RT, int CT, int NW, int D, int EPI>
+__global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
+  constexpr int P = D + 1;
+  constexpr int FA = 2 * RT;                         // activation fragments per stage (plane, row tile)
+  constexpr int DPW = FA / NW;                       // activation loads per wave per stage
+  static_assert(FA % NW == 0, "activation fragments per wave");
+  constexpr int PER = DPW + CT;                      // loads per wave per stage
+  constexpr unsigned SLOT = FA * 1024;
+  extern __shared__ __align__(1024) unsigned char smem[];
+  const int per = (nwg + 7) / 8;
+  const int blk = (blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (blk >= a.total_items) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const void* Wg = a.g[0].W;
+  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroups; ++i) {
+    if (i < a.ngroups && a.g[i].item0 <= blk) {
+      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
+    }
+  }
+  // items of a group: ((split, row chunk), column block), column blocks
+  // fastest, so the workgroups an XCD runs together share one activation
+  // block in its L2
+  const int ncol = a.N / (NW * CT * 16);
+  const int idx = blk - item0;
+  const int nb = idx % ncol;
+  const int sm = idx / ncol;
+  const int mc = sm % n_mc, s = sm / n_mc;
+  const int KS = a.K >> 5;
+  const int ks0 = (s * KS) / a.S, nk = ((s + 1) * KS) / a.S - ks0;
+  const int rbase = row0 + mc * RT * 16;
+  const int rend = row0 + nrows;
+  const int nrt = min(RT, (rend - rbase + 15) >> 4); // row tiles holding rows (the rest are padding:
+                                                     // still loaded, so every wave's load count per
+                                                     // stage stays PER, but neither read nor multiplied)
+  const int nt0 = (nb * NW + w) * CT;                // this wave's first 16-column weight tile
+
+  const unsigned char* asrc[DPW];
+#pragma unroll
+  for (int i = 0; i < DPW; ++i) {
+    const int f = w * DPW + i;
+    const int p = f / RT, r = f % RT;
+    const int row = min(rbase + 16 * r + (lane & 15), rend - 1);
+    asrc[i] = (const unsigned char*)((const uint16_t*)a.X + (size_t)p * a.x_lo + (size_t)row * a.K +
+                                     (size_t)ks0 * 32 + 8 * (lane >> 4));
+  }
+  const u32x4* bsrc = (const u32x4*)Wg + ((size_t)nt0 * KS + ks0) * 64 + lane;
+  const size_t btile = (size_t)KS * 64;              // u32x4 between weight tiles
+  auto issueA = [&](int st) {
+    unsigned char* sl = smem + (st % P) * SLOT;
+#pragma unroll
+    for (int i = 0; i < DPW; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + (size_t)st * 64), MOA_LDS(sl + (w * DPW + i) * 1024),
+                                       16, 0, 0);
+  };
+
+  f32x4_t acc[RT][CT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r)
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc[r][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 breg[D][CT];
+#pragma unroll
+  for (int d = 0; d < D; ++d)
+    if (d < nk) {
+      issueA(d);
+#pragma unroll
+      for (int c = 0; c < CT; ++c) breg[d][c] = bsrc[c * btile + (size_t)d * 64];
+    }
+  const unsigned lbase = lds_addr(smem) + lane * 16;
+  for (int st0 = 0; st0 < nk; st0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int st = st0 + d;
+      if (st < nk) {
+        // stage st resident; every wave done with stage st - 1, whose slot is refilled next
+        if (st + D - 1 < nk) wait_vmcnt<(D - 1) * PER>(); else wait_vmcnt<0>();
+        wait_lgkm0();
+        asm volatile("s_barrier" ::: "memory");
+        if (st + D < nk) issueA(st + D);
+        const unsigned sb = lbase + (unsigned)(st % P) * SLOT;
+        u32x4 ah[RT], al[RT];
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+          if (r < nrt) ah[r] = ds_read_b128(sb + r * 1024);
+        wait_lgkm0();
+#pragma unroll
+        for (int r = 0; r < RT; ++r) tie(ah[r]);
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+          if (r < nrt) al[r] = ds_read_b128(sb + (RT + r) * 1024);
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+          if (r < nrt) {
+#pragma unroll
+            for (int c = 0; c < CT; ++c)
+              acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ah[r]),
+                                                                  __builtin_bit_cast(bf16x8_t, breg[d][c]), acc[r][c], 0, 0, 0);
+          }
+        wait_lgkm0();
+#pragma unroll
+        for (int r = 0; r < RT; ++r) tie(al[r]);
+#pragma unroll
+        for (int r = 0; r < RT; ++r)
+          if (r < nrt) {
+#pragma unroll
+            for (int c = 0; c < CT; ++c)
+              acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, al[r]),
+                                                                  __builtin_bit_cast(bf16x8_t, breg[d][c]), acc[r][c], 0, 0, 0);
+          }
+        if (st + D < nk) {
+#pragma unroll
+          for (int c = 0; c < CT; ++c) breg[d][c] = bsrc[c * btile + (size_t)(st + D) * 64];
+        }
+      }
+    }
+  }
+
+  const int col = lane & 15;
+  const int rq = (lane >> 4) * 4;
+  if (EPI == EPI_F32) {
+    float* out = a.out + (size_t)s * a.out_split;
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int c = 0; c < CT; ++c)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = rbase + r * 16 + rq + i;
+          if (row < rend) out[(size_t)row * a.N + (nt0 + c) * 16 + col] = acc[r][c][i];
+        }
+  } else {
+    // tiles (2p, 2p+1) are (gate, up) of the same 16 hidden units
+    const int half = a.N >> 1;
+#pragma unroll
+    for (int r = 0; r < RT; ++r)
+#pragma unroll
+      for (int q = 0; q < CT / 2; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = rbase + r * 16 + rq + i;
+          if (row < rend) {
+            const float g = acc[r][2 * q][i], u = acc[r][2 * q + 1][i];
+            store_split(a.hout, a.h_lo, (size_t)row * half + ((nt0 >> 1) + q) * 16 + col, g / (1.f + __expf(-g)) * u);
+          }
+        }
   }
 }
 
@@ -1434,19 +1509,6 @@ hipError_t launch_add_rmsnorm(hipStream_t st, bool bf16, float* x, const float* 
   return hipGetLastError();
 }
 
-template <int MT, int NT, int EPI>
-static void gemm_u(hipStream_t st, const GemmArgs& a, int blocks) {
-  if (a.ksteps % 8 == 0) klaunch(k_gemm_bf16<MT, NT, EPI, 8>, dim3(blocks), dim3(256), st, a);
-  else klaunch(k_gemm_bf16<MT, NT, EPI, 4>, dim3(blocks), dim3(256), st, a);
-}
-
-template <int MT>
-static void gemm_nt(hipStream_t st, const GemmArgs& a, int blocks, int epi, int nt) {
-  if (epi == EPI_SWIGLU) gemm_u<MT, 2, EPI_SWIGLU>(st, a, blocks);
-  else if (nt == 2) gemm_u<MT, 2, EPI_F32>(st, a, blocks);
-  else gemm_u<MT, 1, EPI_F32>(st, a, blocks);
-}
-
 template <int WM, int WN, int P, int EPI>
 static hipError_t gemm_big(hipStream_t st, const GemmArgs& a) {
   constexpr int BM = 64 * WM, BN = 128 * WN;
@@ -1463,8 +1525,44 @@ static hipError_t gemm_big(hipStream_t st, const GemmArgs& a) {
   return hipGetLastError();
 }
 
+template <int RT, int CT, int NW, int D, int EPI>
+static hipError_t gemm_mm(hipStream_t st, const GemmArgs& a) {
+  constexpr unsigned shm = 2 * RT * 1024 * (D + 1);
+  static bool attr = false;                           // one attribute call per instantiation
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_mm<RT, CT, NW, D, EPI>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int nwg = a.total_items;
+  klaunch_shm(k_gemm_mm<RT, CT, NW, D, EPI>, dim3((nwg + 7) / 8 * 8), dim3(64 * NW), shm, st, a, nwg);
+  return hipGetLastError();
+}
+
+template <int RT, int EPI>
+static hipError_t gemm_mm_ct(hipStream_t st, const GemmArgs& a, int nt) {
+  if (nt == 4) return gemm_mm<RT, 4, 4, (RT >= 8 ? 2 : 3), EPI>(st, a);
+  if (nt == 2) return gemm_mm<RT, 2, 4, 4, EPI>(st, a);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt) {
   if (a.total_items <= 0) return hipSuccess;
+  if (bf16 && mt > kMmTile && mt <= kMmTile + 8) {   // medium-M: 16*RT rows x (64 nt) columns per workgroup
+    const int rt = mt - kMmTile;
+    if (a.S < 1 || a.S > (a.K >> 5) || a.N % (64 * nt) != 0) return hipErrorInvalidValue;
+    if (epi == EPI_SWIGLU) {
+      if (rt == 2) return gemm_mm_ct<2, EPI_SWIGLU>(st, a, nt);
+      if (rt == 4) return gemm_mm_ct<4, EPI_SWIGLU>(st, a, nt);
+      if (rt == 8) return gemm_mm_ct<8, EPI_SWIGLU>(st, a, nt);
+    } else {
+      if (rt == 2) return gemm_mm_ct<2, EPI_F32>(st, a, nt);
+      if (rt == 4) return gemm_mm_ct<4, EPI_F32>(st, a, nt);
+      if (rt == 8) return gemm_mm_ct<8, EPI_F32>(st, a, nt);
+    }
+    return hipErrorInvalidValue;
+  }
   if (bf16 && mt == kBigTile) {                       // 128 x (128 nt) tiles on the 32x32 MFMA
     if (nt == 2) return epi == EPI_SWIGLU ? gemm_big<2, 2, 4, EPI_SWIGLU>(st, a) : gemm_big<2, 2, 4, EPI_F32>(st, a);
     if (nt == 4) return epi == EPI_SWIGLU ? gemm_big<2, 4, 3, EPI_SWIGLU>(st, a) : gemm_big<2, 4, 3, EPI_F32>(st, a);
@@ -1492,11 +1590,7 @@ hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, in
     klaunch(k_gemm_f32, dim3(a.total_items), dim3(256), st, a);
     return hipGetLastError();
   }
-  const int blocks = (a.total_items + 3) / 4;
-  if (mt == 1) gemm_nt<1>(st, a, blocks, epi, nt);
-  else if (mt == 2) gemm_nt<2>(st, a, blocks, epi, nt);
-  else gemm_nt<4>(st, a, blocks, epi, nt);
-  return hipGetLastError();
+  return hipErrorInvalidValue;                        // no bf16 kernel for this tile code
 }
 
 hipError_t launch_swiglu_f32(hipStream_t st, const float* gu, float* h, int T, int ffn) {

@@ -172,11 +172,12 @@ class Feeder:
     only, whatever the caller's step windows are."""
 
     def __init__(self, eng, workload, expert_models, agg_model=-1, on_step=None, gate_tau=None,
-                 answer_of=None, order="first-seen", window=None):
+                 answer_of=None, order="first-seen", window=None, on_submit=None):
         if window is not None and window < 1:
             raise ValueError("window must be >= 1")
         self.eng, self.wl, self.experts, self.agg = eng, workload, list(expert_models), agg_model
         self.on_step = on_step
+        self.on_submit = on_submit    # on_submit(request id, query, model id, max_new) after each submit
         self.answer_of = answer_of
         self.tau = None if gate_tau is None else Fraction(gate_tau).limit_denominator(64)
         self.window = window
@@ -201,6 +202,8 @@ class Feeder:
         self.res.rid_of[(q, model)] = rid
         self.who[rid] = (q, model, e)
         self.submitted += 1
+        if self.on_submit is not None:
+            self.on_submit(rid, q, model, G)
 
     def _top_up(self):
         n = 0
@@ -266,10 +269,11 @@ class Feeder:
 
 
 def run_feeder(eng, workload, expert_models, agg_model=-1, on_step=None, max_steps=None,
-               gate_tau=None, answer_of=None, order="first-seen", window=None):
+               gate_tau=None, answer_of=None, order="first-seen", window=None, on_submit=None):
     """Drive ``eng`` through ``workload`` (a moa_inputs.Workload) to the end,
     or for at most max_steps engine steps; see Feeder for the arguments."""
-    f = Feeder(eng, workload, expert_models, agg_model, on_step, gate_tau, answer_of, order, window)
+    f = Feeder(eng, workload, expert_models, agg_model, on_step, gate_tau, answer_of, order, window,
+               on_submit)
     f.advance(max_steps)
     return f.res
 

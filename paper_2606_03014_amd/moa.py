@@ -79,7 +79,7 @@ _SIGS = {
     "moa_debug_block_table": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_int32), C.c_int32, P(C.c_int32)]),
     "moa_debug_chunks": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_int64), C.c_int32, P(C.c_int32)]),
     "moa_debug_steps": (C.c_int, [C.c_void_p, P(C.c_int64), C.c_int64, P(C.c_int64)]),
-    "moa_debug_capture_logits": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_float)]),
+    "moa_debug_capture_logits": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_float), C.c_int64]),
     "moa_debug_time_kernels": (C.c_int, [C.c_void_p, C.c_int32, C.c_double, C.c_double]),
     "moa_debug_kernel_stats": (C.c_int, [C.c_void_p, P(moa_kernel_stats)]),
     "moa_debug_measure_peaks": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double)]),
@@ -251,8 +251,12 @@ def moa_debug_steps(eng):
 
 
 def moa_debug_capture_logits(eng, rid, host_array):
-    """host_array: float32 numpy array of max_new_tokens * vocab, kept alive by the caller."""
-    check(lib().moa_debug_capture_logits(eng, rid, host_array.ctypes.data_as(P(C.c_float))),
+    """host_array: contiguous float32 numpy array of at least max_new_tokens *
+    vocab elements, kept alive by the caller until the request is collected."""
+    import numpy as np
+    if host_array.dtype != np.float32 or not host_array.flags.c_contiguous:
+        raise ValueError("capture buffer must be a contiguous float32 array")
+    check(lib().moa_debug_capture_logits(eng, rid, host_array.ctypes.data_as(P(C.c_float)), host_array.size),
           "moa_debug_capture_logits")
 
 

@@ -8,6 +8,13 @@ from oracle import transformer as T
 from paper_2606_03014_amd import Engine
 
 MARGIN = 1e-3          # a token may differ only where the oracle's top-2 margin is below this
+# A bf16 engine keeps its K/V cache in bf16, which alone moves logits by
+# several 1e-2 against a model with an exact cache (measured in the oracle:
+# 2.8e-2 at 1B shape / 16 layers, 4.0e-2 at 8B width / 4 layers, more at
+# 8B / 32 layers; the engine measured 0.131 there). The 2e-2 logit bound is
+# therefore checked against the oracle with a bf16 K/V cache, and the
+# distance to the exact-cache oracle against this looser bound.
+PURE_TOL = 2e-1
 
 
 def say(msg):
@@ -61,17 +68,22 @@ def compare(shape, weights, prompt, toks, logits, bf16_kv, logit_tol, n_layers=N
     """Teacher-forced oracle on the engine's own history; returns (max logit err, flips).
 
     A bf16 engine stores its KV cache in bf16, so its oracle stores K/V in
-    bf16 too (``bf16_kv``); logits and tokens are judged against that oracle.
-    The distance to the oracle with an exact cache is reported, not bounded."""
+    bf16 too (``bf16_kv``); logits (``logit_tol``) and tokens are judged
+    against that oracle, and the distance to the oracle with an exact cache
+    is bounded by PURE_TOL."""
     om = T.OracleModel(shape, weights, n_layers=n_layers, cache=False)
     ref = T.teacher_forced_logits(om, prompt, toks, bf16_kv=bf16_kv)
     assert logits is None or np.all(np.isfinite(logits)), f"{what}: non-finite logits"
     err = float(np.abs(logits - ref).max()) if logits is not None else 0.0
     msg = f"{what}: |engine - oracle| {err:.3e}"
+    perr = None
     if bf16_kv and report_pure and logits is not None:
         pure = T.teacher_forced_logits(om, prompt, toks)
-        msg += f"  (vs oracle with an exact KV cache: {float(np.abs(logits - pure).max()):.3e})"
+        perr = float(np.abs(logits - pure).max())
+        msg += (f"  (vs oracle with an exact KV cache: {perr:.3e}; the oracle's own bf16-cache "
+                f"effect: {float(np.abs(ref - pure).max()):.3e})")
     say(msg)
     assert err <= logit_tol, f"{what}: max |logit - oracle| = {err:.3e} > {logit_tol}"
+    assert perr is None or perr <= PURE_TOL, f"{what}: max |logit - exact-cache oracle| = {perr:.3e} > {PURE_TOL}"
     flips = check_tokens(ref, toks, what)
     return err, flips

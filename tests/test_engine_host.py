@@ -90,6 +90,50 @@ def test_feeder_in_blocks_matches_one_run_and_counts_every_token():
     assert runs[0] == runs[1] == runs[2]
 
 
+def test_capture_logits_checks_its_capacity():
+    """moa_debug_capture_logits takes the buffer's size in floats and refuses
+    one below max_new_tokens * vocab (nothing registered), and refuses a
+    request whose prefill has completed."""
+    c = CONFIGS["tiny-moa-fp32"]
+    eng = _dry(c.model, c.engine, 1, dtype="f32")
+    rid = eng.submit(np.arange(10, dtype=np.int32), 0, 5)
+    with pytest.raises(M.MoaError) as err:
+        eng.capture_logits(rid, np.zeros(5 * c.model.vocab - 1, dtype=np.float32))
+    assert err.value.code == M.MOA_EINVAL
+    with pytest.raises(ValueError):
+        eng.capture_logits(rid, np.zeros(5 * c.model.vocab, dtype=np.float64))
+    buf = np.zeros(5 * c.model.vocab, dtype=np.float32)
+    eng.capture_logits(rid, buf)
+    eng.step()
+    with pytest.raises(M.MoaError) as err:
+        eng.capture_logits(rid, buf)
+    assert err.value.code == M.MOA_ESTATE
+    eng.close()
+
+
+@pytest.mark.parametrize("field,value", [("vocab", 32016), ("n_kv_heads", 1), ("head_dim", 64)])
+def test_bf16_widths_must_be_whole_128_column_tiles(field, value):
+    """A bf16 engine takes only projection widths that are whole 128-column
+    GEMM tiles (LM head = vocab, qkv = (heads + 2 kv heads) x head_dim):
+    anything else is refused at moa_arena_bytes / moa_create."""
+    from dataclasses import replace as rp
+    from paper_2606_03014_amd.engine import engine_cfg
+    c = CONFIGS["moa-4x1b-bf16"]
+    base = ModelShape(n_layers=2, d_model=256, n_heads=5, n_kv_heads=2, head_dim=64, ffn_dim=512, vocab=1024) \
+        if field != "vocab" else c.model
+    if field == "vocab":
+        shape = rp(base, vocab=value)
+    elif field == "n_kv_heads":          # (5 + 2) * 64 = 448: not a multiple of 128
+        shape = rp(base, n_heads=5, n_kv_heads=1)
+    else:                                # (5 + 4) * 64 = 576
+        shape = rp(base, n_heads=5, n_kv_heads=2)
+    with pytest.raises(M.MoaError) as err:
+        M.moa_arena_bytes(engine_cfg(shape, "bf16", c.engine, 1))
+    assert err.value.code == M.MOA_EINVAL
+    ok = rp(c.model, vocab=32000)
+    assert M.moa_arena_bytes(engine_cfg(ok, "bf16", c.engine, 1)) > 0
+
+
 def test_second_model_stream_reserves_one_partial_buffer():
     """A bf16 engine reserves split-K partials for its second model stream in
     the arena; MOA_FLAG_ONE_STREAM drops exactly that buffer, and fp32
