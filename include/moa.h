@@ -178,6 +178,24 @@ moa_status moa_submit_with_history(moa_engine* e, int32_t model_id, int32_t seed
  * or running. EHIP on a runtime failure. */
 moa_status moa_step(moa_engine* e, moa_step_info* info);
 
+/* moa_step for callers that cannot allocate (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation): the same step --
+ * the same plan and kernels, bit-identical results -- that calls no HIP
+ * allocation routine (no hipMalloc / hipHostMalloc / hipFree /
+ * hipEventCreate). Its kernels' split-K and split-KV partial sums live in the
+ * library's static per-GPU scratch array (64 MiB, one copy on each GPU the
+ * library runs on, held until the process ends) instead of the arena; the
+ * metadata goes through the pinned staging sized at moa_create; prompts and
+ * block lists are uploaded from the engine's own host copies; kernel timing
+ * (moa_debug_time_kernels) is skipped for these steps.
+ * ENOMEM, with nothing changed: the engine's planned partials (split-K
+ * partials of every model stream plus split-KV slots) exceed 64 MiB (then
+ * use moa_step). Every moa_step_noalloc on one GPU shares that GPU's array:
+ * calls whose steps overlap on the device (engines stepping on different
+ * streams at once) race; steps of one engine are ordered by its stream.
+ * Other errors as moa_step. */
+moa_status moa_step_noalloc(moa_engine* e, moa_step_info* info);
+
 /* Return requests retired at steps <= upto_step (upto_step < 0: every step
  * enqueued so far) that were not collected yet, in retirement order (step,
  * then admission order), waiting for that step to finish on the device.

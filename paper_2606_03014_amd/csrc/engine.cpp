@@ -240,6 +240,7 @@ struct moa_engine {
   void* xl = nullptr;                 // LM-head input rows (final norm output)
   float* pacc = nullptr;
   float* pml = nullptr;
+  void* scratch = nullptr;            // this GPU's library scratch array (moa_step_noalloc)
 
   // pinned staging ring and per-step completion events
   struct Stage { char* buf = nullptr; size_t cap = 0; };
@@ -248,6 +249,9 @@ struct moa_engine {
   int64_t ev_step[kStageSlots] = {-1, -1, -1, -1};
   int32_t* pinned_out = nullptr;
   size_t pinned_out_cap = 0;
+  // host prompt copies an allocation-free step uploads straight from, kept
+  // until the step that read them completes (released when its slot is reused)
+  std::vector<std::vector<int32_t>> keepalive[kStageSlots];
 
   // kernel timing (inspection hook): event pairs around launches of sampled steps
   struct Timed { int cls, cls2; hipEvent_t a, b; double bytes, flops; };
@@ -627,6 +631,14 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
         }
       err = hipMemcpy(e->rope, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice);
     }
+    if (err == hipSuccess) err = scratch_address(&e->scratch);
+    // staging slots hold the largest step metadata from the start, so an
+    // allocation-free step never has to grow them
+    for (int i = 0; i < kStageSlots && err == hipSuccess; ++i) {
+      const size_t cap = std::max((size_t)L.meta_ints * 4, (size_t)1 << 20);
+      err = hipHostMalloc((void**)&e->stage[i].buf, cap, hipHostMallocDefault);
+      if (err == hipSuccess) e->stage[i].cap = cap;
+    }
     if (err != hipSuccess) {
       hip_fail(nullptr, err, "moa_create");
       moa_destroy(e);
@@ -891,19 +903,51 @@ int64_t nslots_total(const moa_engine* e) {
   return n;
 }
 
+// Bytes of the library scratch an allocation-free step of this engine may
+// need: split-K partials of every model stream and the split-KV attention
+// partials, at their planned capacities (the plan is the same as moa_step's).
+size_t noalloc_scratch_bytes(const moa_engine* e) {
+  const Layout& L = e->lay;
+  const moa_model_cfg& g = e->cfg.model;
+  const size_t part = align_up((size_t)L.part_cap * 4, 256);
+  const size_t pacc = align_up((size_t)L.slots_cap * g.n_heads * g.head_dim * 4, 256);
+  const size_t pml = align_up((size_t)L.slots_cap * g.n_heads * 2 * 4, 256);
+  return part * (size_t)e->nstreams + pacc + pml;
+}
+
 moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int T, int R,
-                        const int* grp_rows, const int* grp_lm) {
+                        const int* grp_rows, const int* grp_lm, bool noalloc) {
   const moa_model_cfg& g = e->cfg.model;
   const Layout& L = e->lay;
   const int slot = (int)(e->step_idx % kStageSlots);
   moa_status st = wait_slot(e, slot);
   if (st != MOA_OK) return st;
+  e->keepalive[slot].clear();                 // the step that read them has completed
+
+  // partial sums: the arena's workspace, or this GPU's library scratch
+  float* part = e->part;
+  float* xpart[kMaxShares - 1];
+  for (int k = 0; k < kMaxShares - 1; ++k) xpart[k] = e->xpart[k];
+  float* pacc = e->pacc;
+  float* pml = e->pml;
+  if (noalloc) {
+    char* sc = (char*)e->scratch;
+    const size_t pb = align_up((size_t)L.part_cap * 4, 256);
+    part = (float*)sc;
+    for (int k = 0; k < kMaxShares - 1; ++k) xpart[k] = k + 1 < e->nstreams ? (float*)(sc + pb * (k + 1)) : nullptr;
+    pacc = (float*)(sc + pb * e->nstreams);
+    pml = (float*)(sc + pb * e->nstreams + align_up((size_t)L.slots_cap * g.n_heads * g.head_dim * 4, 256));
+  }
 
   // ---- stage: metadata, then prompts and block lists of admitted requests
+  // (an allocation-free step stages only the metadata, in the slot sized for
+  // it at moa_create, and uploads prompts and block lists from host copies)
   const int nitems = (int)e->items.size(), nred = (int)e->red.size(), npre = (int)e->pitems.size();
   size_t meta_ints = 4 * (size_t)T + 2 * (size_t)R + 8 * (size_t)nitems + 4 * (size_t)nred + 4 * (size_t)npre;
   size_t up_ints = 0;
-  for (int64_t id : admitted) up_ints += e->reqs[id].prompt.size() + e->reqs[id].blocks.size();
+  if (!noalloc)
+    for (int64_t id : admitted) up_ints += e->reqs[id].prompt.size() + e->reqs[id].blocks.size();
+  if (noalloc && e->stage[slot].cap < meta_ints * 4) return hip_fail(e, hipErrorOutOfMemory, "staging size");
   st = ensure_stage(e, slot, (meta_ints + up_ints) * 4);
   if (st != MOA_OK) return st;
   int* hb = (int*)e->stage[slot].buf;
@@ -921,6 +965,16 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   HIPCHK(hipMemcpyAsync(e->meta, hb, meta_ints * 4, hipMemcpyHostToDevice, e->stream), "meta upload");
   for (int64_t id : admitted) {
     Request& r = e->reqs[id];
+    if (noalloc) {
+      // r.blocks lives as long as the request; the prompt copy until this step completes
+      HIPCHK(hipMemcpyAsync(e->tok_store + r.tok_off, r.prompt.data(), r.prompt.size() * 4, hipMemcpyHostToDevice,
+                            e->stream), "prompt upload");
+      HIPCHK(hipMemcpyAsync(e->bt_store + r.bt_off, r.blocks.data(), r.blocks.size() * 4, hipMemcpyHostToDevice,
+                            e->stream), "block list upload");
+      e->keepalive[slot].push_back(std::move(r.prompt));
+      r.prompt = std::vector<int32_t>();
+      continue;
+    }
     const size_t a = o;
     put(r.prompt.data(), r.prompt.size());
     HIPCHK(hipMemcpyAsync(e->tok_store + r.tok_off, hb + a, r.prompt.size() * 4, hipMemcpyHostToDevice, e->stream),
@@ -970,7 +1024,8 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   }
   auto weights = [&](auto get) { GemmPlanIn w = gin; for (int k = 0; k < w.ngroups; ++k) w.W[k] = get(e->models[gmodel[k]]); return w; };
 
-  e->time_now = e->time_every > 0 && (e->step_idx % e->time_every) == 0;
+  // kernel timing takes events from a pool that may grow: never in an allocation-free step
+  e->time_now = !noalloc && e->time_every > 0 && (e->step_idx % e->time_every) == 0;
   if (e->time_now && e->timed.size() > 16384) {
     moa_status rs = resolve_timed(e);
     if (rs != MOA_OK) return rs;
@@ -1006,7 +1061,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   for (int u = 0; u < nshare; ++u) {
     Share& b = sh[u];
     b.st = u == 0 ? e->stream : e->xs[u - 1];
-    b.part = u == 0 ? e->part : e->xpart[u - 1];
+    b.part = u == 0 ? part : xpart[u - 1];
     b.r0 = e->sh_row[u];
     b.nr = e->sh_row[u + 1] - e->sh_row[u];
     b.g0 = e->sh_group[u];
@@ -1088,10 +1143,10 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
           LAUNCH(MOA_K_ATTN, b.attn_bytes, b.attn_flops,
                  launch_attention(st, bf, b.items, b.nitems, b.max_item_blocks, e->q, e->kv, e->bt_store, sd.row_bt,
                                   l, e->cfg.num_kv_blocks, nh, nkv, hd, 1.0f / std::sqrt((float)hd), e->ao, ao_lo,
-                                  e->pacc, e->pml), "attention");
+                                  pacc, pml), "attention");
         if (b.nred > 0)
           LAUNCH(MOA_K_ATTN_REDUCE, b.red_bytes, 0,
-                 launch_attn_reduce(st, bf, b.red, b.nred, e->pacc, e->pml, e->ao, ao_lo, nh, hd), "attn reduce");
+                 launch_attn_reduce(st, bf, b.red, b.nred, pacc, pml, e->ao, ao_lo, nh, hd), "attn reduce");
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), b.g0, b.ng, nh * hd, d, EPI_F32, e->ao,
                   ao_lo, b.part, nullptr, 0, true, ga, mt, nt);
         gemm_cost(ga, EPI_F32, gb, gf);
@@ -1170,9 +1225,11 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
 
 }  // namespace
 
-moa_status moa_step(moa_engine* e, moa_step_info* info) {
-  if (!e) return MOA_EINVAL;
-  if (e->broken) return MOA_ESTATE;
+}  // extern "C"
+
+namespace {
+
+moa_status step_impl(moa_engine* e, moa_step_info* info, bool noalloc) {
   if (info) std::memset(info, 0, sizeof(*info));
   if (e->pending.empty() && e->running.empty()) {
     if (info) { info->step = -1; info->free_blocks = (int32_t)e->free_blocks.nfree; }
@@ -1390,7 +1447,7 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
       std::fprintf(stderr, "moa: step plan exceeds workspace (T=%d R=%d slots=%d)\n", T, R, nslots);
       return MOA_EHIP;
     }
-    moa_status st = enqueue_step(e, admitted, T, R, grp_rows, grp_lm);
+    moa_status st = enqueue_step(e, admitted, T, R, grp_rows, grp_lm, noalloc);
     if (st != MOA_OK) return st;
     for (auto& cr : capture_rows) {
       Request& r = e->reqs[cr.first];
@@ -1437,6 +1494,26 @@ moa_status moa_step(moa_engine* e, moa_step_info* info) {
     info->emitted = R;
   }
   return MOA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+moa_status moa_step(moa_engine* e, moa_step_info* info) {
+  if (!e) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  return step_impl(e, info, false);
+}
+
+moa_status moa_step_noalloc(moa_engine* e, moa_step_info* info) {
+  if (!e) return MOA_EINVAL;
+  if (e->broken) return MOA_ESTATE;
+  if (noalloc_scratch_bytes(e) > kScratchBytes) {
+    if (info) std::memset(info, 0, sizeof(*info));
+    return MOA_ENOMEM;
+  }
+  return step_impl(e, info, true);
 }
 
 moa_status moa_collect(moa_engine* e, int64_t upto_step, moa_result* res, int32_t cap, int32_t* n_out,

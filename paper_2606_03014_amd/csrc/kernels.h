@@ -126,6 +126,14 @@ hipError_t launch_kv_fill(hipStream_t st, bool bf16, void* kv, const int* blocks
 hipError_t launch_argmax(hipStream_t st, const float* logits, int R, int V, const int* lm_dst,
                          int* tok_store);
 
+// The library's per-GPU scratch array (a file-scope __device__ array of
+// kScratchBytes, one copy on every GPU the library runs on, kept until the
+// process ends): scratch_address() looks its device address up once per
+// device (the current one) and returns it. moa_step_noalloc puts its
+// kernels' partial sums there.
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+hipError_t scratch_address(void** out);
+
 // Peak microbenchmarks (peaks.hip). read: every byte of [p, p + bytes) once;
 // sink needs `grid` words. mfma: grid workgroups of 4 waves, 4 * iters
 // 32x32x16 bf16 MFMAs per wave; sink needs grid * 256 floats.

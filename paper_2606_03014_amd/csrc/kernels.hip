@@ -12,8 +12,31 @@
 #include <hip/hip_runtime.h>
 #include <climits>
 #include <cmath>
+#include <mutex>
 
 namespace moa {
+
+// Scratch for the kernels of allocation-free calls: partial sums only (every
+// byte is written before it is read within a call, so nothing is cleared).
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+hipError_t scratch_address(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return err;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return err;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 // Optional event pair attached to the next launch (hipExtLaunchKernel
 // timestamps the dispatch itself, so the measured span is the kernel's).

@@ -63,6 +63,9 @@ class Engine:
     def step(self):
         return M.moa_step(self.h)
 
+    def step_noalloc(self):
+        return M.moa_step_noalloc(self.h)
+
     def collect(self, upto=-1):
         return M.moa_collect(self.h, upto)
 

@@ -70,6 +70,7 @@ _SIGS = {
     "moa_submit_with_history": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p, C.c_int32,
                                           P(C.c_int64)]),
     "moa_step": (C.c_int, [C.c_void_p, P(moa_step_info)]),
+    "moa_step_noalloc": (C.c_int, [C.c_void_p, P(moa_step_info)]),
     "moa_collect": (C.c_int, [C.c_void_p, C.c_int64, P(moa_result), C.c_int32, P(C.c_int32),
                               P(C.c_int32), C.c_int64]),
     "moa_sync": (C.c_int, [C.c_void_p]),
@@ -169,6 +170,12 @@ def moa_submit_with_history(eng, model_id, seed_token, ctx_len, max_new_tokens, 
 def moa_step(eng):
     info = moa_step_info()
     check(lib().moa_step(eng, C.byref(info)), "moa_step")
+    return info
+
+
+def moa_step_noalloc(eng):
+    info = moa_step_info()
+    check(lib().moa_step_noalloc(eng, C.byref(info)), "moa_step_noalloc")
     return info
 
 

@@ -134,6 +134,33 @@ def test_bf16_widths_must_be_whole_128_column_tiles(field, value):
     assert M.moa_arena_bytes(engine_cfg(ok, "bf16", c.engine, 1)) > 0
 
 
+def test_step_noalloc_plans_like_step_and_refuses_oversized_partials():
+    """The allocation-free step plans exactly like moa_step (same bookkeeping
+    on a dry run); an engine whose planned partials exceed the library's
+    64 MiB scratch is refused with MOA_ENOMEM before anything changes."""
+    c = CONFIGS["tiny-moa-fp32"]
+    wl = make_workload(c.name, 0)
+    traces = []
+    for noalloc in (False, True):
+        eng = _dry(c.model, c.engine, 3, dtype="f32")
+        for q, e, G in wl.expert_requests():
+            eng.submit(wl.prompts[q], e, G)
+        while (eng.step_noalloc() if noalloc else eng.step()).step >= 0:
+            pass
+        traces.append(eng.steps().tolist())
+        eng.close()
+    assert traces[0] == traces[1] and len(traces[0]) > 10
+    big = CONFIGS["moa-3+1x8b-bf16"]
+    eng = _dry(big.model, big.engine, 4)
+    eng.submit(np.arange(20, dtype=np.int32), 0, 3)
+    with pytest.raises(M.MoaError) as err:
+        eng.step_noalloc()
+    assert err.value.code == M.MOA_ENOMEM
+    assert len(eng.steps()) == 0
+    assert eng.step().step == 0
+    eng.close()
+
+
 def test_second_model_stream_reserves_one_partial_buffer():
     """A bf16 engine reserves split-K partials for its second model stream in
     the arena; MOA_FLAG_ONE_STREAM drops exactly that buffer, and fp32
