@@ -124,7 +124,11 @@ moa_status moa_arena_bytes(const moa_engine_cfg* cfg, size_t* bytes);
 moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_bytes,
                       void* hip_stream, moa_engine** out);
 
-/* Load one model. host_weights is the packed blob: tensors in the order
+/* Load one model (Section "MOSAIC: Multi-Model Scheduling", subsection
+ * "Problem Setting": the deployment draws its experts from a pool of
+ * heterogeneous models; here every expert and the aggregator are resident
+ * at once, so the per-model load cost l_m of that subsection is paid once,
+ * here, instead of per session). host_weights is the packed blob: tensors in the order
  *   embed[V,d], { attn_norm[d], wq[nh*hd,d], wk[nkv*hd,d], wv[nkv*hd,d],
  *   wo[d,nh*hd], mlp_norm[d], w_gate[ffn,d], w_up[ffn,d], w_down[d,ffn] } x L,
  *   final_norm[d], lm_head[V,d]
@@ -137,8 +141,11 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
 moa_status moa_load_expert(moa_engine* e, const moa_model_cfg* cfg, const void* host_weights,
                            size_t nbytes, int32_t* model_id);
 
-/* Queue one generation call: prompt tokens[0..n_tokens) for model model_id,
- * emitting exactly max_new_tokens tokens. Request ids are dense and increase
+/* Queue one generation call (subsection "Problem Setting": the fixed prompt
+ * set, routed before scheduling, is a batch of (prompt, expert) calls;
+ * subsection "MOSAIC: Adaptive Aggregation": the aggregator call is one more
+ * such call on the query followed by the expert outputs): prompt
+ * tokens[0..n_tokens) for model model_id, emitting exactly max_new_tokens tokens. Request ids are dense and increase
  * in submit order. The request waits in a FIFO until its KV blocks
  * ceil((n_tokens + max_new_tokens - 1) / 16) and a seat are free.
  * EINVAL: n_tokens < 1, max_new_tokens < 1, unknown model, token id outside
@@ -165,7 +172,11 @@ moa_status moa_submit(moa_engine* e, const int32_t* tokens, int32_t n_tokens, in
 moa_status moa_submit_with_history(moa_engine* e, int32_t model_id, int32_t seed_token, int32_t ctx_len,
                                    const void* host_kv, int32_t max_new_tokens, int64_t* request_id);
 
-/* Plan one step on the host and enqueue its kernels on the stream:
+/* Plan one step on the host and enqueue its kernels on the stream (the
+ * generation phase that subsection "Workload Characterisation" makes the
+ * dominant cost, run as continuous batching of every resident model's calls,
+ * which appendix "The Pitfalls of Data Concurrency and Over-Sharding" needs
+ * to keep decode bound by memory bandwidth):
  *   1 admit FIFO heads while a seat and their blocks are free (head-of-line
  *     blocking); a request gets the smallest free block ids, ascending;
  *   2 prefill: running requests in admission order take prompt positions up
@@ -196,7 +207,9 @@ moa_status moa_step(moa_engine* e, moa_step_info* info);
  * Other errors as moa_step. */
 moa_status moa_step_noalloc(moa_engine* e, moa_step_info* info);
 
-/* Return requests retired at steps <= upto_step (upto_step < 0: every step
+/* Hand back finished calls (subsection "MOSAIC: Adaptive Aggregation": the
+ * expert outputs a query's aggregator call, or the confidence gate of Eq. 11,
+ * is waiting for). Return requests retired at steps <= upto_step (upto_step < 0: every step
  * enqueued so far) that were not collected yet, in retirement order (step,
  * then admission order), waiting for that step to finish on the device.
  * Tokens are written back to back into tok_buf. If cap or tok_cap is too

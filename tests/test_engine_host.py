@@ -336,6 +336,36 @@ def test_hand_traced_example_matches():
         assert [list(c) for c in eng.chunks(rid)] == want["chunks"]
 
 
+def test_hand_traced_windowed_feeder_matches():
+    """The engine's feeder with a submission window of one call reproduces
+    the hand trace (aggregator calls overtake an unsubmitted expert call)."""
+    f = GOLD["feeder_window"]
+    consts = EngineConsts(f["num_blocks"], f["max_num_seqs"], f["max_prefill_tokens"], 1000)
+    eng = _dry(TOY, consts, f["n_models"])
+    nq = len(f["queries"])
+
+    class W:
+        prompts = [np.ones(q["P"], dtype=np.int32) for q in f["queries"]]
+        experts = [tuple(e for e, _ in q["experts"]) for q in f["queries"]]
+        max_new = {(qi, e): G for qi, q in enumerate(f["queries"]) for e, G in q["experts"]}
+        n_experts = 2
+        n_queries = nq
+        agg_max_new = f["agg_G"]
+
+        def expert_requests(self):
+            return [(q, e, self.max_new[(q, e)]) for q in range(nq) for e in self.experts[q]]
+
+    r = run_feeder(eng, W(), [0, 1], agg_model=f["aggregator"], window=f["window"])
+    assert eng.steps().tolist() == f["steps"]
+    assert [[a, list(b)] for a, b in r.collects] == f["collects"]
+    for rid, want in enumerate(f["requests"]):
+        info = eng.request(rid)
+        assert (info.model_id, info.prompt_len, info.max_new_tokens, info.admit_step, info.finish_step) == (
+            want["model"], want["P"], want["G"], want["admit"], want["finish"])
+        assert eng.block_table(rid) == want["blocks"]
+    eng.close()
+
+
 def test_hand_traced_feeder_matches():
     f = GOLD["feeder"]
     consts = EngineConsts(f["num_blocks"], f["max_num_seqs"], f["max_prefill_tokens"], 1000)

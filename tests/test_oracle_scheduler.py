@@ -51,6 +51,24 @@ def test_hand_traced_feeder():
             want["model"], want["P"], want["G"], want["admit"], want["finish"], want["blocks"])
 
 
+def test_hand_traced_windowed_feeder():
+    """The feeder's submission window, traced by hand: with W = 1 the
+    aggregator calls of q0 and q1 overtake q2's unsubmitted expert call."""
+    f = GOLD["feeder_window"]
+    s = OracleScheduler(f["num_blocks"], f["max_num_seqs"], f["max_prefill_tokens"], f["n_models"])
+    calls = [(q, e, qq["P"], G) for q, qq in enumerate(f["queries"]) for e, G in qq["experts"]]
+    log, _ = run_feeder(s, calls, agg_model=f["aggregator"], agg_G=f["agg_G"],
+                        query_len=[qq["P"] for qq in f["queries"]],
+                        query_experts=[tuple(e for e, _ in qq["experts"]) for qq in f["queries"]],
+                        window=f["window"])
+    assert [list(t) for t in s.steps] == f["steps"]
+    assert [[a, list(b)] for a, b in log] == f["collects"]
+    assert len(s.reqs) == len(f["requests"])
+    for r, want in zip(s.reqs, f["requests"]):
+        assert (r.expert, r.P, r.G, r.admit_step, r.finish_step, r.blocks) == (
+            want["model"], want["P"], want["G"], want["admit"], want["finish"], want["blocks"])
+
+
 def test_submit_validation():
     s = OracleScheduler(4, 2, 16, 2)
     for bad in [(2, 5, 3), (-1, 5, 3), (0, 0, 3), (0, 5, 0)]:
