@@ -578,6 +578,7 @@ def schedule_study(args, cfg):
 
 
 def main():
+    t_start = time.perf_counter()
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20, help="timed bench steps")
@@ -698,6 +699,7 @@ def main():
             out["cpu_baseline"] = cpu_baseline_history(cfg, args.seed, weights0)
         else:
             out["cpu_baseline"] = cpu_baseline(cfg, wl, weights0)
+    log(f"[bench] whole run {time.perf_counter() - t_start:.1f} s (models, peaks, warm-up, timed steps, CPU leg)")
     print(json.dumps(out), flush=True)
 
 
