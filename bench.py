@@ -512,67 +512,137 @@ def calibrate_placement(args, cfg):
                       "placements_K2": plans, "workload": cfg.name}), flush=True)
 
 
+def plan_cost(cfg):
+    """Per-unit costs of the schedule cost model for cfg's model shape."""
+    import numpy as np
+    from moa_inputs.weights import tensor_shapes
+    g = cfg.model
+    esz = 2 if cfg.dtype == "bf16" else 4
+    n_params = sum(int(np.prod(sh)) for _, sh in tensor_shapes(g))
+    return {"streamed": (n_params - g.vocab * g.d_model) * esz,          # every matrix but the embedding
+            "kv_per_ctx": 2 * g.n_layers * g.n_kv_heads * g.head_dim * esz,
+            "lin_flops": 2.0 * (n_params - g.vocab * g.d_model),           # per prefill token
+            "pair_flops": 4.0 * g.n_heads * g.head_dim * g.n_layers,       # per causal (q, k) pair
+            "blob_bytes": n_params * esz}
+
+
+def price_plan(eng, res, cost, nm):
+    """Model time of a schedule planned by a plan-only engine (res: the
+    feeder's FeedResult). Per step: the weights of every model with a row in
+    the step and the K/V of every decode row's context at STUDY_BW, prefill
+    tokens at the large-M GEMM rate and causal prefill pairs at the
+    prefill-attention rate. Returns (model seconds, steps, generated tokens,
+    mean models per step)."""
+    import numpy as np
+    S = res.n_steps
+    active = np.zeros((S + 1, nm), bool)
+    ctx = np.zeros(S + 1)
+    pre = np.zeros(S + 1)
+    pairs = 0.0
+    gen = 0
+    for (q, m), rid in res.rid_of.items():
+        info = eng.request(rid)
+        ch = eng.chunks(rid)
+        for s, a, b in ch:
+            pre[s] += b
+            pairs += b * a + b * (b + 1) / 2
+            active[s, m] = True
+        d0 = max(s for s, a, b in ch) + 1       # decode steps d0..finish, at positions P..P+G-2
+        d1 = info.finish_step
+        if d1 >= d0:
+            active[d0:d1 + 1, m] = True
+            ctx[d0:d1 + 1] += info.prompt_len + 1 + np.arange(d1 - d0 + 1)
+        gen += info.max_new_tokens
+    t = (active.sum(axis=1) * cost["streamed"] + ctx * cost["kv_per_ctx"]) / STUDY_BW + pre * cost["lin_flops"] / STUDY_LIN
+    model_s = float(t.sum() + pairs * cost["pair_flops"] / STUDY_ATTN)
+    return model_s, S, gen, float(active[:S].sum(axis=1).mean())
+
+
+def plan_only_run(cfg, wl, consts, order="first-seen", window=None, gate=None):
+    """The workload's schedule on a plan-only engine (no GPU); gate: a dict
+    of Feeder gate arguments. Returns price_plan's tuple."""
+    import numpy as np
+    from paper_2606_03014_amd import Engine, run_feeder
+    nm = cfg.n_experts + (1 if cfg.aggregator else 0)
+    cost = plan_cost(cfg)
+    eng = Engine(cfg.model, cfg.dtype, consts, nm, plan_only=True)
+    blob = np.zeros(cost["blob_bytes"], np.uint8)
+    for _ in range(nm):
+        eng.load(blob)
+    r = run_feeder(eng, wl, list(range(cfg.n_experts)), agg_model=cfg.n_experts if cfg.aggregator else -1,
+                   order=order, window=window, **(gate or {}))
+    out = price_plan(eng, r, cost, nm)
+    eng.close()
+    return out + (r,)
+
+
 def schedule_study(args, cfg):
     """Plan-only schedules of the workload under the feeder's policies
     (submission order x submission window x prefill budget), with no GPU: the
     engine's own scheduler plans every step, and a per-step cost model prices
-    it. Per step: the weights of every model with a row in the step at
-    STUDY_BW, the K/V of every decode row's context at STUDY_BW, prefill
-    tokens at the measured large-M GEMM rate and causal prefill pairs at the
-    measured prefill-attention rate. Prints one JSON line."""
+    it (price_plan). Prints one JSON line."""
     import dataclasses
-    import numpy as np
     from moa_inputs import make_workload
-    from moa_inputs.weights import tensor_shapes
-    from paper_2606_03014_amd import Engine, run_feeder
-    g = cfg.model
-    esz = 2 if cfg.dtype == "bf16" else 4
-    n_params = sum(int(np.prod(sh)) for _, sh in tensor_shapes(g))
-    streamed = (n_params - g.vocab * g.d_model) * esz           # every matrix but the embedding
-    kv_per_ctx = 2 * g.n_layers * g.n_kv_heads * g.head_dim * esz
-    lin_flops = 2.0 * (n_params - g.vocab * g.d_model)           # per prefill token
-    pair_flops = 4.0 * g.n_heads * g.head_dim * g.n_layers       # per causal (q, k) pair
     wl = make_workload(cfg.name, args.seed, n_queries=args.queries)
-    nm = cfg.n_experts + (1 if cfg.aggregator else 0)
-    blob = np.zeros(n_params * esz, np.uint8)
     rows_out = []
     for order in ("first-seen", "longest-first"):
         for window in (None, 256, 64, 16):
             for budget in (4096, 16384, 32768):
                 consts = dataclasses.replace(cfg.engine, max_prefill_tokens=budget)
-                eng = Engine(g, cfg.dtype, consts, nm, plan_only=True)
-                for _ in range(nm):
-                    eng.load(blob)
-                r = run_feeder(eng, wl, list(range(cfg.n_experts)), agg_model=cfg.n_experts if cfg.aggregator else -1,
-                               order=order, window=window)
-                S = r.n_steps
-                active = np.zeros((S + 1, nm), bool)
-                ctx = np.zeros(S + 1)
-                pre = np.zeros(S + 1)
-                pairs = 0.0
-                gen = 0
-                for (q, m), rid in r.rid_of.items():
-                    info = eng.request(rid)
-                    ch = eng.chunks(rid)
-                    for s, a, b in ch:
-                        pre[s] += b
-                        pairs += b * a + b * (b + 1) / 2
-                        active[s, m] = True
-                    d0 = max(s for s, a, b in ch) + 1       # decode steps d0..finish, at positions P..P+G-2
-                    d1 = info.finish_step
-                    if d1 >= d0:
-                        active[d0:d1 + 1, m] = True
-                        ctx[d0:d1 + 1] += info.prompt_len + 1 + np.arange(d1 - d0 + 1)
-                    gen += info.max_new_tokens
-                t = (active.sum(axis=1) * streamed + ctx * kv_per_ctx) / STUDY_BW + pre * lin_flops / STUDY_LIN
-                model_s = float(t.sum() + pairs * pair_flops / STUDY_ATTN)
-                eng.close()
+                model_s, S, gen, act, _ = plan_only_run(cfg, wl, consts, order, window)
                 rows_out.append({"order": order, "window": window, "prefill_budget": budget, "steps": S,
                                  "model_s": float(f"{model_s:.4g}"), "model_tokens_per_s": round(gen / model_s),
-                                 "mean_active_models": round(float(active[:S].sum(axis=1).mean()), 3)})
+                                 "mean_active_models": round(act, 3)})
                 log(f"[bench] {order:13s} window {str(window):5s} budget {budget:6d}: {S} steps, "
                     f"model {model_s:.1f} s")
     print(json.dumps({"schedule_study": rows_out, "workload": cfg.name, "queries": wl.n_queries,
+                      "cost_model": {"stream_Bps": STUDY_BW, "prefill_linear_flops": STUDY_LIN,
+                                     "prefill_attention_flops": STUDY_ATTN}}), flush=True)
+
+
+def policy_study(args, cfg, eng, mids):
+    """The feeder's policies measured on the GPU (Section "MOSAIC: Multi-Model
+    Scheduling" for the order, Eq. 11 / Algorithm 1 for the gate): the same
+    query slice run to completion under first-seen and longest-first
+    submission, and under first-seen with the confidence gate at tau = 1
+    for two synthetic answer spaces (an expert's answer is its first token
+    mod A, so about 1/A of the two-expert queries agree). Each measured
+    makespan stands beside the plan-only cost model's for the same schedule
+    (for a gated run, planned with the GPU run's own answers). Prints one
+    JSON line."""
+    import torch
+    from moa_inputs import make_workload
+    from paper_2606_03014_amd import Feeder
+    wl = make_workload(cfg.name, args.seed, n_queries=args.queries or 256)
+    agg = mids[cfg.n_experts] if cfg.aggregator else -1
+    rows = []
+    for order, A in (("first-seen", None), ("longest-first", None), ("first-seen", 2), ("first-seen", 8)):
+        gate = {}
+        if A:
+            gate = dict(gate_tau=1, answer_of=lambda q, e, toks, A=A: int(toks[0]) % A)
+        prog = Progress()
+        f = Feeder(eng, wl, mids[: cfg.n_experts], agg_model=agg, on_step=prog, order=order, **gate)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        f.advance(None)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        r = f.res
+        pgate = {}
+        if A:
+            ans = {(q, e): int(r.outputs[(q, mids[e])][0]) % A for q in range(wl.n_queries) for e in wl.experts[q]}
+            pgate = dict(gate_tau=1, answer_of=lambda q, e, toks, ans=ans: ans[(q, e)])
+        model_s, S, gen, act, pr = plan_only_run(cfg, wl, cfg.engine, order, None, pgate)
+        assert S == r.n_steps and pr.agg_calls == r.agg_calls, "plan-only and GPU schedules differ"
+        rows.append({"order": order, "gate": {"tau": 1, "answer_options": A} if A else None,
+                     "makespan_s": wall, "engine_steps": r.n_steps, "generated_tokens": r.tokens,
+                     "tokens_per_s": r.tokens / wall, "aggregator_calls": r.agg_calls,
+                     "gated_queries": len(r.gated), "model_makespan_s": model_s,
+                     "model_over_measured": model_s / wall})
+        log(f"[bench] policy {order} gate A={A}: {r.n_steps} steps, {r.tokens} tokens, {wall:.1f} s "
+            f"(model {model_s:.1f} s), aggregator calls {r.agg_calls}, gated {len(r.gated)}")
+    print(json.dumps({"policy_study": rows, "workload": cfg.name, "queries": wl.n_queries, "seed": args.seed,
+                      "model_streams": 1 if eng.cfg.flags & 2 else 2,
                       "cost_model": {"stream_Bps": STUDY_BW, "prefill_linear_flops": STUDY_LIN,
                                      "prefill_attention_flops": STUDY_ATTN}}), flush=True)
 
@@ -598,6 +668,9 @@ def main():
                     help="submission order of the expert calls")
     ap.add_argument("--calibrate-placement", action="store_true",
                     help="fit the per-model session cost on this engine and solve the placement ILP for 1..8 workers")
+    ap.add_argument("--policy-study", action="store_true",
+                    help="measure the feeder's policies (order, confidence gate) to completion on a query slice "
+                         "(default 256 queries) beside the plan-only cost model")
     ap.add_argument("--schedule-study", action="store_true",
                     help="plan-only schedules under each submission order, window and prefill budget, "
                          "priced by a per-step cost model (no GPU)")
@@ -647,6 +720,10 @@ def main():
     mids, weights0 = load_models(eng, cfg, args.seed, n_models)
     read_bps, mfma_fps = eng.measure_peaks()
     log(f"[bench] measured peaks: HBM read {read_bps / 1e12:.2f} TB/s, bf16 32x32x16 MFMA {mfma_fps / 1e15:.2f} PFLOP/s")
+    if args.policy_study:
+        policy_study(args, cfg, eng, mids)
+        eng.close()
+        return
     run = bench_straggler if straggler else bench_feeder
     tokens, wall, config, extra, wl = run(args, cfg, eng, mids)
     stats = eng.kernel_stats()
