@@ -466,33 +466,47 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
     a.total_items = item;
     return;
   }
-  // Medium row counts: the medium-M kernel (whole 16-row tiles of a group
-  // per workgroup, 256 columns, weights streamed through registers), sized
-  // so the grid stays resident (two to three workgroups per CU: 300..768
-  // items). Measured against the workgroup-tile kernel on 8B shapes with
-  // cold weights: 10-40% faster for the F32 projections once a group has
-  // more than 24 rows; for gate-up (no k-split: the SwiGLU epilogue needs the
-  // whole sum) only while the row chunks give 300..768 items.
-  if (maxM > 24 && N % 256 == 0) {
-    const int rt = maxM <= 32 ? 2 : 4;
-    const int ncol = N / 256;
-    int chunks = 0;
-    for (int g = 0; g < in.ngroups; ++g) chunks += (in.nrows[g] + 16 * rt - 1) / (16 * rt);
-    const int base = chunks * ncol;
+  // Medium row counts (17 and up per model, below the large-M thresholds):
+  // the medium-M kernel, whole 16-row tiles of a group per workgroup
+  // (RT tiles: 2 up to 32 rows, 4 up to 64, else 8 per row chunk), 8 waves
+  // over 512 columns where N allows (4 waves over 256 and at most 4 row
+  // tiles otherwise), and about one workgroup per CU: F32 projections take
+  // the k-split that brings the grid nearest ~224 workgroups; gate-up (no
+  // k-split: its SwiGLU epilogue needs the whole sum) the first tile shape
+  // whose grid has 150..256 workgroups, else the workgroup-tile kernel.
+  // Measured on 8B shapes with cold weights, three groups of 16..200 rows:
+  // 2-40% faster per projection than the workgroup-tile kernel, and
+  // bit-identical on the same split.
+  if (maxM > 16 && N % 256 == 0) {
+    struct Shape { int rt, nw, ct; };
+    auto chunks_of = [&](int rt) {
+      int c = 0;
+      for (int g = 0; g < in.ngroups; ++g) c += (in.nrows[g] + 16 * rt - 1) / (16 * rt);
+      return c;
+    };
+    const int rt0 = maxM <= 32 ? 2 : (maxM <= 64 ? 4 : 8);
+    Shape sh{0, 0, 0};
     int S = 1;
-    bool use = false;
     if (epi == EPI_SWIGLU) {
-      use = base >= 300 && base <= 768;
+      const int rtb = std::max(rt0, 4);
+      const Shape cand[4] = {{rtb, 8, 4}, {rtb == 8 ? 8 : 0, 8, 2}, {4, 4, 4}, {2, 4, 4}};
+      for (const Shape& c : cand) {
+        if (c.rt == 0 || N % (16 * c.nw * c.ct)) continue;
+        const int items = chunks_of(c.rt) * (N / (16 * c.nw * c.ct));
+        if (items >= 150 && items <= 256) { sh = c; break; }
+      }
     } else {
-      use = true;
+      sh = (rt0 >= 4 && N % 512 == 0) ? Shape{rt0, 8, 4} : Shape{std::min(rt0, 4), 4, 4};
       if (allow_split) {
-        S = std::max(1, std::min(16, (512 + base / 2) / std::max(base, 1)));
+        const int base = chunks_of(sh.rt) * (N / (16 * sh.nw * sh.ct));
+        S = std::max(1, std::min(16, (224 + base / 2) / std::max(base, 1)));
         while (S > 1 && ((int64_t)S * totalM * N > e->lay.part_cap || S > KS)) --S;
       }
     }
-    if (use) {
-      mt = kMmTile + rt;
-      nt = 4;
+    if (sh.rt) {
+      const int ncol = N / (16 * sh.nw * sh.ct);
+      mt = kMmTile + sh.rt;
+      nt = sh.nw == 8 ? 8 + sh.ct : sh.ct;
       a.S = S;
       a.ksteps = KS / S;                   // informational: split s takes k-steps [s*KS/S, (s+1)*KS/S)
       a.out_split = (size_t)totalM * N;
@@ -500,7 +514,7 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
       for (int k = 0; k < ng; ++k) {
         const int g = g0 + k;
         a.g[k].W = in.W[g]; a.g[k].row0 = in.row0[g]; a.g[k].nrows = in.nrows[g];
-        a.g[k].n_mc = (in.nrows[g] + 16 * rt - 1) / (16 * rt);
+        a.g[k].n_mc = (in.nrows[g] + 16 * sh.rt - 1) / (16 * sh.rt);
         a.g[k].item0 = item;
         item += a.g[k].n_mc * S * ncol;
       }

@@ -47,9 +47,11 @@ constexpr int kWgTile = 1000;
 // MFMA; each item is 128 rows x 128*nt columns x one k-split
 // (N % (128*nt) == 0, K % 32 == 0, ksteps >= 1).
 constexpr int kBigTile = 2000;
-// launch_gemm(mt = kMmTile + RT, nt = CT): the medium-M kernel; each item is
-// 16*RT rows (RT = 2, 4 or 8) x 64*CT columns (CT = 2 or 4) x one of S
-// k-splits of K/32/S k-steps (rounded; 1 <= S <= K/32, N % (64*CT) == 0).
+// launch_gemm(mt = kMmTile + RT, nt): the medium-M kernel; each item is 16*RT
+// rows (RT = 2, 4 or 8) x NW*CT*16 columns x one of S k-splits of K/32/S
+// k-steps (rounded; 1 <= S <= K/32), with nt = CT (NW = 4 waves; CT = 2 or 4)
+// or nt = 8 + CT (NW = 8 waves; CT = 4 with RT >= 4, CT = 2 with RT = 8);
+// N must be a multiple of the columns.
 constexpr int kMmTile = 3000;
 
 // Attention work item: one query row against keys [k0, k1) of its request.

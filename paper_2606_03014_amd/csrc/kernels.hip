@@ -662,19 +662,40 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) 
 //    workgroups fit on a CU: the planner keeps the whole grid resident at once
 //    (a grid of more items than slots ran at half the streaming rate in its
 //    last, partly empty round).
-//  * Per stage a wave multiplies the hi plane while the lo plane's fragments
-//    are read; the RT x CT accumulators form that many independent MFMA
-//    chains (16x16x32 needs about 16 to reach its rate).
+//  * Per stage a wave reads its hi-plane fragments, multiplies them, then the
+//    lo plane (other waves on the SIMD fill the read latency); the RT x CT
+//    accumulators form that many independent MFMA chains (16x16x32 needs
+//    about 16 to reach its rate).
 //  * Loads complete in issue order: stage s's activation loads, then its
 //    weight loads, so waiting until D - 1 stages' worth of loads are
 //    outstanding makes stage s resident.
 //  * k-splits take KS / S k-steps each, rounded (any S).
-__device__ __forceinline__ u32x4 ds_read_b128(unsigned addr) {
-  u32x4 v;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
-  return v;
+// N 16-byte LDS reads at addr + OFF + 1024 * i and the wait for them, in
+// one asm statement: the compiler sees the registers only once they hold
+// the data (an asm read whose wait came later let it copy a register that
+// was still in flight when registers were scarce).
+template <int N, int OFF>
+__device__ __forceinline__ void lds_frags(u32x4 (&v)[N], unsigned addr) {
+  static_assert(N == 2 || N == 4 || N == 8, "fragment count");
+  if constexpr (N == 2) {
+    asm volatile("ds_read_b128 %0, %2 offset:%3\n\tds_read_b128 %1, %2 offset:%4\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(v[0]), "=&v"(v[1]) : "v"(addr), "i"(OFF), "i"(OFF + 1024));
+  } else if constexpr (N == 4) {
+    asm volatile("ds_read_b128 %0, %4 offset:%5\n\tds_read_b128 %1, %4 offset:%6\n\t"
+                 "ds_read_b128 %2, %4 offset:%7\n\tds_read_b128 %3, %4 offset:%8\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3])
+                 : "v"(addr), "i"(OFF), "i"(OFF + 1024), "i"(OFF + 2048), "i"(OFF + 3072));
+  } else {
+    asm volatile("ds_read_b128 %0, %8 offset:%9\n\tds_read_b128 %1, %8 offset:%10\n\t"
+                 "ds_read_b128 %2, %8 offset:%11\n\tds_read_b128 %3, %8 offset:%12\n\t"
+                 "ds_read_b128 %4, %8 offset:%13\n\tds_read_b128 %5, %8 offset:%14\n\t"
+                 "ds_read_b128 %6, %8 offset:%15\n\tds_read_b128 %7, %8 offset:%16\n\ts_waitcnt lgkmcnt(0)"
+                 : "=&v"(v[0]), "=&v"(v[1]), "=&v"(v[2]), "=&v"(v[3]), "=&v"(v[4]), "=&v"(v[5]), "=&v"(v[6]),
+                   "=&v"(v[7])
+                 : "v"(addr), "i"(OFF), "i"(OFF + 1024), "i"(OFF + 2048), "i"(OFF + 3072), "i"(OFF + 4096),
+                   "i"(OFF + 5120), "i"(OFF + 6144), "i"(OFF + 7168));
+  }
 }
-__device__ __forceinline__ void tie(u32x4& v) { asm volatile("" : "+v"(v)); }
 
 template <int RT, int CT, int NW, int D, int EPI>
 __global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
@@ -725,12 +746,23 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
   }
   const u32x4* bsrc = (const u32x4*)Wg + ((size_t)nt0 * KS + ks0) * 64 + lane;
   const size_t btile = (size_t)KS * 64;              // u32x4 between weight tiles
+  // Every stage issues the same loads, past the last stage too (clamped to
+  // it; those activation copies land in ring slots nobody reads again and
+  // the weight copies are dropped), so the number of loads in flight is the
+  // same at every wait and the compiler never has to drain the whole queue
+  // to make a register of the ring safe to read.
   auto issueA = [&](int st) {
+    const int sk = min(st, nk - 1);
     unsigned char* sl = smem + (st % P) * SLOT;
 #pragma unroll
     for (int i = 0; i < DPW; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + (size_t)st * 64), MOA_LDS(sl + (w * DPW + i) * 1024),
+      __builtin_amdgcn_global_load_lds((const void*)(asrc[i] + (size_t)sk * 64), MOA_LDS(sl + (w * DPW + i) * 1024),
                                        16, 0, 0);
+  };
+  auto loadB = [&](int st, u32x4* dst) {
+    const size_t sk = (size_t)min(st, nk - 1) * 64;
+#pragma unroll
+    for (int c = 0; c < CT; ++c) dst[c] = bsrc[c * btile + sk];
   };
 
   f32x4_t acc[RT][CT];
@@ -741,34 +773,25 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
 
   u32x4 breg[D][CT];
 #pragma unroll
-  for (int d = 0; d < D; ++d)
-    if (d < nk) {
-      issueA(d);
-#pragma unroll
-      for (int c = 0; c < CT; ++c) breg[d][c] = bsrc[c * btile + (size_t)d * 64];
-    }
+  for (int d = 0; d < D; ++d) {
+    issueA(d);
+    loadB(d, breg[d]);
+  }
   const unsigned lbase = lds_addr(smem) + lane * 16;
   for (int st0 = 0; st0 < nk; st0 += D) {
 #pragma unroll
     for (int d = 0; d < D; ++d) {
       const int st = st0 + d;
+      // stage st resident (D - 1 newer stages in flight); every wave done
+      // with stage st - 1, whose slot is refilled next
+      wait_vmcnt<(D - 1) * PER>();
+      wait_lgkm0();
+      asm volatile("s_barrier" ::: "memory");
+      issueA(st + D);
       if (st < nk) {
-        // stage st resident; every wave done with stage st - 1, whose slot is refilled next
-        if (st + D - 1 < nk) wait_vmcnt<(D - 1) * PER>(); else wait_vmcnt<0>();
-        wait_lgkm0();
-        asm volatile("s_barrier" ::: "memory");
-        if (st + D < nk) issueA(st + D);
         const unsigned sb = lbase + (unsigned)(st % P) * SLOT;
         u32x4 ah[RT], al[RT];
-#pragma unroll
-        for (int r = 0; r < RT; ++r)
-          if (r < nrt) ah[r] = ds_read_b128(sb + r * 1024);
-        wait_lgkm0();
-#pragma unroll
-        for (int r = 0; r < RT; ++r) tie(ah[r]);
-#pragma unroll
-        for (int r = 0; r < RT; ++r)
-          if (r < nrt) al[r] = ds_read_b128(sb + (RT + r) * 1024);
+        lds_frags<RT, 0>(ah, sb);
 #pragma unroll
         for (int r = 0; r < RT; ++r)
           if (r < nrt) {
@@ -777,9 +800,7 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
               acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ah[r]),
                                                                   __builtin_bit_cast(bf16x8_t, breg[d][c]), acc[r][c], 0, 0, 0);
           }
-        wait_lgkm0();
-#pragma unroll
-        for (int r = 0; r < RT; ++r) tie(al[r]);
+        lds_frags<RT, RT * 1024>(al, sb);
 #pragma unroll
         for (int r = 0; r < RT; ++r)
           if (r < nrt) {
@@ -788,13 +809,11 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
               acc[r][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, al[r]),
                                                                   __builtin_bit_cast(bf16x8_t, breg[d][c]), acc[r][c], 0, 0, 0);
           }
-        if (st + D < nk) {
-#pragma unroll
-          for (int c = 0; c < CT; ++c) breg[d][c] = bsrc[c * btile + (size_t)(st + D) * 64];
-        }
       }
+      loadB(st + D, breg[d]);
     }
   }
+  wait_vmcnt<0>();                                   // no load may land in LDS after the workgroup ends
 
   const int col = lane & 15;
   const int rq = (lane >> 4) * 4;
@@ -1563,26 +1582,33 @@ static hipError_t gemm_mm(hipStream_t st, const GemmArgs& a) {
   return hipGetLastError();
 }
 
+// nt: CT (4 waves) or 8 + CT (8 waves); see kMmTile
 template <int RT, int EPI>
-static hipError_t gemm_mm_ct(hipStream_t st, const GemmArgs& a, int nt) {
+static hipError_t gemm_mm_nt(hipStream_t st, const GemmArgs& a, int nt) {
   if (nt == 4) return gemm_mm<RT, 4, 4, (RT >= 8 ? 2 : 3), EPI>(st, a);
   if (nt == 2) return gemm_mm<RT, 2, 4, 4, EPI>(st, a);
+  if constexpr (RT >= 4) {
+    if (nt == 12) return gemm_mm<RT, 4, 8, (RT >= 8 ? 2 : 3), EPI>(st, a);
+    if constexpr (RT >= 8)
+      if (nt == 10) return gemm_mm<RT, 2, 8, 3, EPI>(st, a);
+  }
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, int mt, int nt) {
   if (a.total_items <= 0) return hipSuccess;
-  if (bf16 && mt > kMmTile && mt <= kMmTile + 8) {   // medium-M: 16*RT rows x (64 nt) columns per workgroup
+  if (bf16 && mt > kMmTile && mt <= kMmTile + 8) {   // medium-M: 16*RT rows x (16 * NW * CT) columns
     const int rt = mt - kMmTile;
-    if (a.S < 1 || a.S > (a.K >> 5) || a.N % (64 * nt) != 0) return hipErrorInvalidValue;
+    const int cols = nt > 8 ? 8 * 16 * (nt - 8) : 4 * 16 * nt;
+    if (a.S < 1 || a.S > (a.K >> 5) || a.N % cols != 0) return hipErrorInvalidValue;
     if (epi == EPI_SWIGLU) {
-      if (rt == 2) return gemm_mm_ct<2, EPI_SWIGLU>(st, a, nt);
-      if (rt == 4) return gemm_mm_ct<4, EPI_SWIGLU>(st, a, nt);
-      if (rt == 8) return gemm_mm_ct<8, EPI_SWIGLU>(st, a, nt);
+      if (rt == 2) return gemm_mm_nt<2, EPI_SWIGLU>(st, a, nt);
+      if (rt == 4) return gemm_mm_nt<4, EPI_SWIGLU>(st, a, nt);
+      if (rt == 8) return gemm_mm_nt<8, EPI_SWIGLU>(st, a, nt);
     } else {
-      if (rt == 2) return gemm_mm_ct<2, EPI_F32>(st, a, nt);
-      if (rt == 4) return gemm_mm_ct<4, EPI_F32>(st, a, nt);
-      if (rt == 8) return gemm_mm_ct<8, EPI_F32>(st, a, nt);
+      if (rt == 2) return gemm_mm_nt<2, EPI_F32>(st, a, nt);
+      if (rt == 4) return gemm_mm_nt<4, EPI_F32>(st, a, nt);
+      if (rt == 8) return gemm_mm_nt<8, EPI_F32>(st, a, nt);
     }
     return hipErrorInvalidValue;
   }
