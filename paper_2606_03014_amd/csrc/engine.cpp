@@ -603,7 +603,7 @@ moa_status moa_create(const moa_engine_cfg* cfg, void* dev_arena, size_t arena_b
   e->free_blocks.init(cfg->num_kv_blocks);
   e->model_top = L.off_models;
   // a dry run plans the model-stream shares a GPU engine would use
-  if (plan_only && L.off_xpart[0]) e->nstreams = 1 + (int)std::count_if(L.off_xpart, L.off_xpart + kMaxShares - 1, [](size_t o) { return o != 0; });
+  if (plan_only && L.off_xpart[0]) e->nstreams = 1 + (int)std::count_if(L.off_xpart, L.off_xpart + (kMaxShares - 1), [](size_t o) { return o != 0; });
   if (!plan_only) {
     e->stream = (hipStream_t)hip_stream;
     e->arena = (char*)dev_arena;

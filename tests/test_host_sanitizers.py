@@ -1,0 +1,70 @@
+"""The engine's host code under AddressSanitizer and UndefinedBehaviorSanitizer.
+
+engine.cpp (admission, paged blocks, chunked prefill, step plans and their
+model-stream shares, retire/collect, the inspection hooks and every
+documented error return) is compiled with both sanitizers on its host side
+and linked, with the normally built kernel objects, into a small C program
+that drives MOA_FLAG_PLAN_ONLY engines through the C ABI
+(tests/sanitize/plan_driver.c). A plan-only engine makes no HIP call, so this
+runs without a GPU. The oracle is Python (numpy) and has no native code to
+sanitize.
+"""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2606_03014_amd", "csrc")
+BUILD = os.path.join(CSRC, "_build")
+LLVM = "/opt/rocm/llvm/bin"
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+SAN = ["address", "undefined"]
+
+
+def _run(cmd, **kw):
+    r = subprocess.run(cmd, capture_output=True, text=True, **kw)
+    assert r.returncode == 0, " ".join(cmd) + "\n" + r.stdout[-4000:] + r.stderr[-4000:]
+    return r
+
+
+@pytest.fixture(scope="module")
+def driver(tmp_path_factory):
+    if not (os.path.exists(HIPCC) and os.path.exists(os.path.join(LLVM, "clang"))):
+        pytest.skip("ROCm toolchain not found")
+    from paper_2606_03014_amd.build import FLAGS, build
+    objs = [os.path.join(BUILD, s + ".o") for s in ("kernels.hip", "peaks.hip")]
+    if not all(os.path.exists(o) for o in objs):
+        build()
+    out = tmp_path_factory.mktemp("san")
+    host_san = []
+    for s in SAN:          # sanitizers on the host side only
+        host_san += ["-Xarch_host", f"-fsanitize={s}"]
+    eng_o = str(out / "engine_san.o")
+    flags = [f for f in FLAGS if f != "-O3"]
+    _run([HIPCC] + flags + ["-O1", "-g", "-Xarch_host", "-fno-omit-frame-pointer",
+                            "-Xarch_host", "-fno-sanitize-recover=all"] + host_san +
+         ["-c", os.path.join(CSRC, "engine.cpp"), "-o", eng_o])
+    drv_o = str(out / "plan_driver.o")
+    san = ",".join(SAN)
+    _run([os.path.join(LLVM, "clang"), "-std=c11", "-O1", "-g", "-Wall", f"-fsanitize={san}",
+          "-fno-sanitize-recover=all", "-I", os.path.join(ROOT, "include"),
+          "-c", os.path.join(ROOT, "tests", "sanitize", "plan_driver.c"), "-o", drv_o])
+    exe = str(out / "plan_driver")
+    _run([os.path.join(LLVM, "clang++"), f"-fsanitize={san}", drv_o, eng_o] + objs +
+         ["-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib", "-o", exe])
+    return exe
+
+
+def test_plan_only_engine_is_clean_under_asan_and_ubsan(driver):
+    env = dict(os.environ)
+    env["ASAN_OPTIONS"] = "detect_leaks=1:abort_on_error=0:halt_on_error=1"
+    env["UBSAN_OPTIONS"] = "print_stacktrace=1:halt_on_error=1"
+    supp = os.path.join(ROOT, "tests", "sanitize", "lsan.supp")
+    env["LSAN_OPTIONS"] = f"suppressions={supp}"
+    r = subprocess.run([driver], capture_output=True, text=True, env=env, timeout=300)
+    log = r.stdout + r.stderr
+    assert r.returncode == 0, log[-6000:]
+    assert "ERROR: AddressSanitizer" not in log and "runtime error" not in log, log[-6000:]
+    assert "plan_driver: ok" in r.stdout
