@@ -469,8 +469,10 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
   // Medium row counts (17 and up per model, below the large-M thresholds):
   // the medium-M kernel, whole 16-row tiles of a group per workgroup
   // (RT tiles: 2 up to 32 rows, 4 up to 64, else 8 per row chunk), 8 waves
-  // over 512 columns where N allows (4 waves over 256 and at most 4 row
-  // tiles otherwise), and about one workgroup per CU: F32 projections take
+  // over 512 columns where N allows (otherwise 8 waves over 256 at RT = 8,
+  // 4 waves over 256 below: a vocabulary of 128,256 is 501 x 256, and two
+  // 64-row chunks per model would stream its LM head twice), and about one
+  // workgroup per CU: F32 projections take
   // the k-split that brings the grid nearest ~224 workgroups; gate-up (no
   // k-split: its SwiGLU epilogue needs the whole sum) the first tile shape
   // whose grid has 150..256 workgroups, else the workgroup-tile kernel.
@@ -496,7 +498,7 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
         if (items >= 150 && items <= 256) { sh = c; break; }
       }
     } else {
-      sh = (rt0 >= 4 && N % 512 == 0) ? Shape{rt0, 8, 4} : Shape{std::min(rt0, 4), 4, 4};
+      sh = (rt0 >= 4 && N % 512 == 0) ? Shape{rt0, 8, 4} : (rt0 == 8 ? Shape{8, 8, 2} : Shape{rt0, 4, 4});
       if (allow_split) {
         const int base = chunks_of(sh.rt) * (N / (16 * sh.nw * sh.ct));
         S = std::max(1, std::min(16, (224 + base / 2) / std::max(base, 1)));

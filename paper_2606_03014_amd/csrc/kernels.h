@@ -49,8 +49,9 @@ constexpr int kWgTile = 1000;
 constexpr int kBigTile = 2000;
 // launch_gemm(mt = kMmTile + RT, nt): the medium-M kernel; each item is 16*RT
 // rows (RT = 2, 4 or 8) x NW*CT*16 columns x one of S k-splits of K/32/S
-// k-steps (rounded; 1 <= S <= K/32), with nt = CT (NW = 4 waves; CT = 2 or 4)
-// or nt = 8 + CT (NW = 8 waves; CT = 4 with RT >= 4, CT = 2 with RT = 8);
+// k-steps (rounded; 1 <= S <= K/32), with nt = CT (NW = 4 waves, RT <= 4;
+// CT = 2 or 4) or nt = 8 + CT (NW = 8 waves; CT = 4 with RT >= 4, CT = 2
+// with RT = 8);
 // N must be a multiple of the columns.
 constexpr int kMmTile = 3000;
 

@@ -651,15 +651,17 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) 
 // ------------------------------------------- medium-M GEMM (16x16x32 MFMA)
 // Decode batches put a few dozen to a few hundred rows on each model, so
 // every weight byte feeds only that many rows of MFMA work: the GEMM must
-// stream the weights at HBM speed. A workgroup of 4 waves owns up to 16*RT
+// stream the weights at HBM speed. A workgroup of NW waves owns up to 16*RT
 // rows of one model (all of them, for groups up to that size, so each weight
-// tile leaves HBM once per step) x 4 * CT * 16 columns x one k-split.
+// tile leaves HBM once per step) x NW * CT * 16 columns x one k-split.
 //  * The split-bf16 activation block of a 32-k stage (2*RT fragments of 1 KB,
-//    both planes) is shared by the four waves: it goes HBM/L2 -> LDS by
-//    direct loads into a ring of D + 1 slots.
+//    both planes) is shared by the waves: it goes HBM/L2 -> LDS by direct
+//    loads into a ring of D + 1 slots.
 //  * Each wave streams its own CT weight tiles (1 KB fragments) straight into
-//    a register ring D stages deep, so the LDS holds only activations and two
-//    workgroups fit on a CU: the planner keeps the whole grid resident at once
+//    a register ring D stages deep (a stage's loads are issued once its
+//    registers have fed the MFMAs: issuing them before, from a ring one
+//    stage deeper, measured ~10% slower at 100+ rows), so the LDS holds only
+//    activations: the planner sizes the grid to the resident slots
 //    (a grid of more items than slots ran at half the streaming rate in its
 //    last, partly empty round).
 //  * Per stage a wave reads its hi-plane fragments, multiplies them, then the
@@ -1585,7 +1587,8 @@ static hipError_t gemm_mm(hipStream_t st, const GemmArgs& a) {
 // nt: CT (4 waves) or 8 + CT (8 waves); see kMmTile
 template <int RT, int EPI>
 static hipError_t gemm_mm_nt(hipStream_t st, const GemmArgs& a, int nt) {
-  if (nt == 4) return gemm_mm<RT, 4, 4, (RT >= 8 ? 2 : 3), EPI>(st, a);
+  if constexpr (RT <= 4)                          // 4 waves x RT = 8 x CT = 4: one wave per SIMD
+    if (nt == 4) return gemm_mm<RT, 4, 4, 3, EPI>(st, a);
   if (nt == 2) return gemm_mm<RT, 2, 4, 4, EPI>(st, a);
   if constexpr (RT >= 4) {
     if (nt == 12) return gemm_mm<RT, 4, 8, (RT >= 8 ? 2 : 3), EPI>(st, a);
