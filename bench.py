@@ -600,6 +600,12 @@ def schedule_study(args, cfg):
                                      "prefill_attention_flops": STUDY_ATTN}}), flush=True)
 
 
+# the feeder policies of the study: submission order, and the synthetic
+# answer space of the confidence gate (None: no gate)
+POLICIES = {"first-seen": ("first-seen", None), "longest-first": ("longest-first", None),
+            "gate-A2": ("first-seen", 2), "gate-A8": ("first-seen", 8)}
+
+
 def policy_study(args, cfg, eng, mids):
     """The feeder's policies measured on the GPU (Section "MOSAIC: Multi-Model
     Scheduling" for the order, Eq. 11 / Algorithm 1 for the gate): the same
@@ -616,7 +622,9 @@ def policy_study(args, cfg, eng, mids):
     wl = make_workload(cfg.name, args.seed, n_queries=args.queries or 256)
     agg = mids[cfg.n_experts] if cfg.aggregator else -1
     rows = []
-    for order, A in (("first-seen", None), ("longest-first", None), ("first-seen", 2), ("first-seen", 8)):
+    for name, (order, A) in POLICIES.items():
+        if args.policies and name not in args.policies.split(","):
+            continue
         gate = {}
         if A:
             gate = dict(gate_tau=1, answer_of=lambda q, e, toks, A=A: int(toks[0]) % A)
@@ -634,7 +642,7 @@ def policy_study(args, cfg, eng, mids):
             pgate = dict(gate_tau=1, answer_of=lambda q, e, toks, ans=ans: ans[(q, e)])
         model_s, S, gen, act, pr = plan_only_run(cfg, wl, cfg.engine, order, None, pgate)
         assert S == r.n_steps and pr.agg_calls == r.agg_calls, "plan-only and GPU schedules differ"
-        rows.append({"order": order, "gate": {"tau": 1, "answer_options": A} if A else None,
+        rows.append({"policy": name, "order": order, "gate": {"tau": 1, "answer_options": A} if A else None,
                      "makespan_s": wall, "engine_steps": r.n_steps, "generated_tokens": r.tokens,
                      "tokens_per_s": r.tokens / wall, "aggregator_calls": r.agg_calls,
                      "gated_queries": len(r.gated), "model_makespan_s": model_s,
@@ -671,6 +679,8 @@ def main():
     ap.add_argument("--policy-study", action="store_true",
                     help="measure the feeder's policies (order, confidence gate) to completion on a query slice "
                          "(default 256 queries) beside the plan-only cost model")
+    ap.add_argument("--policies", default=None,
+                    help="comma-separated subset of the policy study's policies (" + ", ".join(POLICIES) + ")")
     ap.add_argument("--schedule-study", action="store_true",
                     help="plan-only schedules under each submission order, window and prefill budget, "
                          "priced by a per-step cost model (no GPU)")
