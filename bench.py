@@ -47,7 +47,7 @@ METRIC = "generated tokens/s on 1 MI355X (ragged MoA batch); attn/GEMM % of HBM/
 STUDY_BW = 5.0e12
 STUDY_LIN = 4.7e14
 STUDY_ATTN = 3.2e14
-DEFAULT_STREAMS = 1
+DEFAULT_STREAMS = 2
 
 
 def log(msg):
@@ -58,7 +58,9 @@ def measured_traffic(kernel, workload, streams=1):
     """HBM bytes per launch of ``kernel`` on ``workload`` from the committed
     rocprofv3 counter summaries, or None when none exists, the kernel source
     changed since, or the counters were taken with another number of model
-    streams (which changes what one launch carries)."""
+    streams (which changes what one launch carries). The roofline's launches
+    are those of the steps sampled for timing, which always run on one
+    stream, so it asks for the one-stream counters."""
     import glob
     import hashlib
     src = os.path.join(ROOT, "paper_2606_03014_amd", "csrc", "kernels.hip")
@@ -737,17 +739,19 @@ def main():
     run = bench_straggler if straggler else bench_feeder
     tokens, wall, config, extra, wl = run(args, cfg, eng, mids)
     stats = eng.kernel_stats()
-    roof = kernel_summary(stats, cfg.name, streams=streams)
+    roof = kernel_summary(stats, cfg.name, streams=1)
     config["model_streams"] = streams
     if roof is not None and streams > 1:
-        roof["overlap"] = ("launch durations from two model streams whose kernels run concurrently: "
-                           "each launch carries half the batch's models and shares the GPU with the "
-                           "other stream's launches (--one-stream times them alone)")
+        roof["timed_steps"] = ("one engine step in --time-every runs every kernel on one stream and is the "
+                               "one timed; the others split their models over two streams")
     from paper_2606_03014_amd.moa import VIEW_CLASSES
     real = {k: v for k, v in stats.items() if k not in VIEW_CLASSES}
     run_roof_ms = sum(s["roof_ms_all"] for s in real.values())
-    # kernel time of every launch, estimated from the timed sample of each class
-    busy_ms = sum(s["ms"] / s["launches"] * s["launches_all"] for s in real.values() if s["launches"])
+    # kernel time of every launch, estimated from the timed sample of each
+    # class in proportion to its bytes (an untimed two-stream launch carries
+    # about half the step's models)
+    busy_ms = sum(s["ms"] * (s["bytes_all"] / s["bytes"] if s["bytes"] > 0 else s["launches_all"] / s["launches"])
+                  for s in real.values() if s["launches"])
 
     out = {
         "metric": METRIC,

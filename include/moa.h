@@ -293,8 +293,8 @@ enum {
  * per (query head, query, visible key). */
 typedef struct {
   int64_t launches;   /* timed launches (sampled steps) */
-  double ms;          /* their summed durations (HIP events on the launch's stream; with two
-                         model streams a launch may share the GPU with the other stream's) */
+  double ms;          /* their summed durations (HIP events around each launch; sampled
+                         steps run on one stream, so no other stream's kernels overlap them) */
   double bytes;       /* their algorithmic bytes */
   double flops;       /* their algorithmic flops */
   int64_t launches_all; /* every launch since the reset */
@@ -305,7 +305,10 @@ typedef struct {
 /* Reset the statistics; from now on account every launch (bytes, flops,
  * roofline time at the given peaks, bytes/s and flop/s) and time every launch
  * of one step out of `every` (every <= 0: no timing) with an event pair
- * around it on the engine's stream. */
+ * around it on the engine's stream. A timed step runs all of its kernels on
+ * the caller's stream (a two-stream engine included; the results are the
+ * same bits), so a timed launch carries the whole step and runs beside no
+ * other stream's kernels. */
 moa_status moa_debug_time_kernels(moa_engine* e, int32_t every, double peak_bw, double peak_flops);
 
 /* Statistics per class, out[MOA_K_COUNT]. Waits for the stream. */

@@ -400,6 +400,14 @@ struct GemmPlanIn {
 // whole step, so a launch that carries only the groups [g0, g0 + ng) plans
 // the same way and writes its partials where the consumer of the whole step
 // expects them); the arguments carry only those groups.
+// A step sampled for kernel timing (one in time_every; never an
+// allocation-free step) runs every kernel on the caller's stream, so each
+// timed launch carries the whole step and no other stream's kernels run
+// beside it: its duration is its own.
+bool step_is_timed(const moa_engine* e, bool noalloc) {
+  return !noalloc && e->time_every > 0 && (e->step_idx % e->time_every) == 0;
+}
+
 void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K, int N, int epi, const void* X,
                size_t x_lo, float* out, uint16_t* hout, size_t h_lo, bool allow_split, GemmArgs& a, int& mt,
                int& nt) {
@@ -1041,7 +1049,7 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
   auto weights = [&](auto get) { GemmPlanIn w = gin; for (int k = 0; k < w.ngroups; ++k) w.W[k] = get(e->models[gmodel[k]]); return w; };
 
   // kernel timing takes events from a pool that may grow: never in an allocation-free step
-  e->time_now = !noalloc && e->time_every > 0 && (e->step_idx % e->time_every) == 0;
+  e->time_now = step_is_timed(e, noalloc);
   if (e->time_now && e->timed.size() > 16384) {
     moa_status rs = resolve_timed(e);
     if (rs != MOA_OK) return rs;
@@ -1305,6 +1313,7 @@ moa_status step_impl(moa_engine* e, moa_step_info* info, bool noalloc) {
   // by set, so each stream's share is one contiguous run.
   int set_size[kMaxShares] = {0};
   int nsets = 1;
+  const int step_streams = step_is_timed(e, noalloc) ? 1 : e->nstreams;
   {
     double cost[kMaxModels] = {0};
     bool active[kMaxModels] = {false};
@@ -1327,7 +1336,7 @@ moa_status step_impl(moa_engine* e, moa_step_info* info, bool noalloc) {
       }
     for (int m = 0; m < M; ++m) e->mcost[m] = cost[m];
     e->nactive = na;
-    nsets = std::max(1, std::min(e->nstreams, na));
+    nsets = std::max(1, std::min(step_streams, na));
     if (nsets > 1) {
       int by_cost[kMaxModels];
       for (int i = 0; i < na; ++i) by_cost[i] = am[i];
@@ -1410,7 +1419,7 @@ moa_status step_impl(moa_engine* e, moa_step_info* info, bool noalloc) {
   // model stream (rows, LM rows and items follow their groups).
   int ngrp = 0;
   for (int m = 0; m < M; ++m) ngrp += grp_rows[m] > 0;
-  const int nshare = std::max(1, std::min(e->nstreams, ngrp));
+  const int nshare = std::max(1, std::min(step_streams, ngrp));
   e->nshare = nshare;
   e->sh_group[0] = 0;
   for (int u = 0; u < nshare; ++u) e->sh_group[u + 1] = e->sh_group[u] + set_size[u];

@@ -22,11 +22,15 @@ def say(msg):
     sys.stdout.flush()
 
 
-def run_requests(shape, dtype, consts, weights_list, requests, capture=True, repeat=1, one_stream=False):
-    """requests: [(tokens, model_index, G)]. Returns (tokens by request, logits by request)."""
+def run_requests(shape, dtype, consts, weights_list, requests, capture=True, repeat=1, one_stream=False,
+                 time_every=0):
+    """requests: [(tokens, model_index, G)]. Returns (tokens by request, logits by request).
+    time_every > 0: kernel timing on one step in time_every (those steps run on one stream)."""
     eng = Engine(shape, dtype, consts, len(weights_list), one_stream=one_stream)
     try:
         mids = [eng.load(pack_blob(w, shape)) for w in weights_list]
+        if time_every:
+            eng.time_kernels(time_every)
         outs, caps = [], []
         for _ in range(repeat):
             cap = {}

@@ -242,6 +242,12 @@ def test_bf16_four_models_two_streams():
         assert np.array_equal(toks[i], toks1[i]), f"req{i}: tokens differ between one and two streams"
         assert np.array_equal(logs[i], logs1[i], equal_nan=True), f"req{i}: logits differ between one and two streams"
     say("four models: one-stream run bit-identical to the two-stream run")
+    # steps sampled for kernel timing run on one stream, the others on two
+    toks2, logs2 = run_requests(SMALL_BF16, "bf16", consts, ws, reqs, time_every=2)
+    for i in range(len(reqs)):
+        assert np.array_equal(toks[i], toks2[i]), f"req{i}: tokens differ with timed one-stream steps"
+        assert np.array_equal(logs[i], logs2[i], equal_nan=True), f"req{i}: logits differ with timed one-stream steps"
+    say("four models: every other step timed on one stream, bit-identical")
 
 
 def test_bf16_runs_are_deterministic():
