@@ -515,6 +515,22 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
     }
     if (sh.rt) {
       const int ncol = N / (16 * sh.nw * sh.ct);
+      // Row chunks of up to T 16-row tiles per group. Gate-up (one k-split)
+      // takes the smallest T, down to 4, whose grid still fits 256
+      // workgroups: a large group's rows then spread over more workgroups
+      // (its split-bf16 MFMA work, not the weight stream, is what holds the
+      // others up from ~5 tiles per workgroup), and the chunks of one weight
+      // column block run side by side on one XCD, which reads it once. The
+      // k-split of the other projections already divides every workgroup.
+      auto tiles = [&](int g) { return (in.nrows[g] + 15) / 16; };
+      int T = sh.rt;
+      if (epi == EPI_SWIGLU)
+        for (int t = sh.rt - 1; t >= 4; --t) {
+          int items = 0;
+          for (int g = 0; g < in.ngroups; ++g) items += (tiles(g) + t - 1) / t * ncol;
+          if (items > 256) break;
+          T = t;
+        }
       mt = kMmTile + sh.rt;
       nt = sh.nw == 8 ? 8 + sh.ct : sh.ct;
       a.S = S;
@@ -524,7 +540,10 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
       for (int k = 0; k < ng; ++k) {
         const int g = g0 + k;
         a.g[k].W = in.W[g]; a.g[k].row0 = in.row0[g]; a.g[k].nrows = in.nrows[g];
-        a.g[k].n_mc = (in.nrows[g] + 16 * sh.rt - 1) / (16 * sh.rt);
+        const int tg = std::max(1, tiles(g));
+        const int nch = (tg + T - 1) / T;
+        a.g[k].mrows = 16 * ((tg + nch - 1) / nch);          // balanced chunks of at most T tiles
+        a.g[k].n_mc = (in.nrows[g] + a.g[k].mrows - 1) / a.g[k].mrows;   // 0 for an empty group
         a.g[k].item0 = item;
         item += a.g[k].n_mc * S * ncol;
       }

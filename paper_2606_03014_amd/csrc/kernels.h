@@ -19,6 +19,8 @@ struct GemmGroup {
   int row0, nrows;  // rows [row0, row0 + nrows) of X and of the output
   int n_mc;         // row chunks of 16*MT rows
   int item0;        // first wave item of this group
+  int mrows;        // medium-M kernel: rows per row chunk (a multiple of 16, at most 16*RT;
+                    // 0: 16*RT); the other kernels ignore it
 };
 
 constexpr int kMaxGroups = kMaxModels;

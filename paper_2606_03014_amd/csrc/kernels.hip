@@ -713,25 +713,27 @@ __global__ __launch_bounds__(64 * NW) void k_gemm_mm(GemmArgs a, int nwg) {
   if (blk >= a.total_items) return;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const void* Wg = a.g[0].W;
-  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
+  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0, mrows = a.g[0].mrows;
 #pragma unroll
   for (int i = 1; i < kMaxGroups; ++i) {
     if (i < a.ngroups && a.g[i].item0 <= blk) {
       Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
+      mrows = a.g[i].mrows;
     }
   }
-  // items of a group: ((split, row chunk), column block), column blocks
-  // fastest, so the workgroups an XCD runs together share one activation
-  // block in its L2
+  // items of a group: ((split, column block), row chunk), row chunks
+  // fastest: the chunks of one weight column block are neighbours, so they
+  // run together on one XCD and its L2 serves the block to all of them
   const int ncol = a.N / (NW * CT * 16);
   const int idx = blk - item0;
-  const int nb = idx % ncol;
-  const int sm = idx / ncol;
-  const int mc = sm % n_mc, s = sm / n_mc;
+  const int mc = idx % n_mc;
+  const int nb = (idx / n_mc) % ncol;
+  const int s = idx / (n_mc * ncol);
   const int KS = a.K >> 5;
   const int ks0 = (s * KS) / a.S, nk = ((s + 1) * KS) / a.S - ks0;
-  const int rbase = row0 + mc * RT * 16;
-  const int rend = row0 + nrows;
+  const int crows = mrows > 0 ? mrows : RT * 16;
+  const int rbase = row0 + mc * crows;
+  const int rend = min(row0 + nrows, rbase + crows);  // this chunk's rows end
   const int nrt = min(RT, (rend - rbase + 15) >> 4); // row tiles holding rows (the rest are padding:
                                                      // still loaded, so every wave's load count per
                                                      // stage stays PER, but neither read nor multiplied)
@@ -1604,6 +1606,8 @@ hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, in
     const int rt = mt - kMmTile;
     const int cols = nt > 8 ? 8 * 16 * (nt - 8) : 4 * 16 * nt;
     if (a.S < 1 || a.S > (a.K >> 5) || a.N % cols != 0) return hipErrorInvalidValue;
+    for (int g = 0; g < a.ngroups; ++g)
+      if (a.g[g].mrows < 0 || a.g[g].mrows % 16 != 0 || a.g[g].mrows > 16 * rt) return hipErrorInvalidValue;
     if (epi == EPI_SWIGLU) {
       if (rt == 2) return gemm_mm_nt<2, EPI_SWIGLU>(st, a, nt);
       if (rt == 4) return gemm_mm_nt<4, EPI_SWIGLU>(st, a, nt);
