@@ -430,6 +430,7 @@ def bench_straggler(args, cfg, eng, mids):
     torch.cuda.synchronize()
     tokens = steps = 0
     phases = []
+    ns0 = time.monotonic_ns()
     t0 = time.perf_counter()
     for i in range(args.steps):
         ts = time.perf_counter()
@@ -450,6 +451,7 @@ def bench_straggler(args, cfg, eng, mids):
             f"{ka} tokens in {ta:.2f} s, drain {tok - ka} tokens in {te - ts - ta:.2f} s; rows "
             f"max {max(rows)} mean {sum(rows) / len(rows):.0f}")
     wall = time.perf_counter() - t0
+    log(f"[bench] timed region monotonic_ns {ns0} {time.monotonic_ns()}")
     config = {"workload": cfg.name, "models": 1, "live_sequences": sw.n_live,
               "refill_steps": sw.refill_steps, "generated_tokens_per_step": tokens // args.steps,
               "engine_steps_per_step": steps // args.steps, "seed": args.seed,
