@@ -334,7 +334,9 @@ def bench_feeder(args, cfg, eng, mids):
                       window=args.window, **gate)
 
     block = args.block_steps if args.block_steps > 0 else None
-    feeder = new_feeder()
+    # one feeder across the blocks of the one schedule; for whole-batch steps
+    # each bench step makes its own (a feeder submits its calls when made)
+    feeder = new_feeder() if block else None
 
     def one_step():
         nonlocal feeder

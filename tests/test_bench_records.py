@@ -52,3 +52,40 @@ def test_bench_refuses_more_than_one_gpu():
                          capture_output=True, text=True, timeout=120)
     assert out.returncode == 2
     assert "one GPU only" in out.stderr and out.stdout == ""
+
+
+def _dry_engine(cfg, n_models):
+    import numpy as np
+    from paper_2606_03014_amd import Engine
+    g = cfg.model
+    qd, kd = g.n_heads * g.head_dim, g.n_kv_heads * g.head_dim
+    n = 2 * g.vocab * g.d_model + g.d_model + g.n_layers * (
+        2 * g.d_model + (qd + 2 * kd) * g.d_model + g.d_model * qd + 3 * g.ffn_dim * g.d_model)
+    eng = Engine(g, cfg.dtype, cfg.engine, n_models, plan_only=True)
+    mids = [eng.load(np.zeros(n * (2 if cfg.dtype == "bf16" else 4), dtype=np.uint8)) for _ in range(n_models)]
+    return eng, mids
+
+
+def test_whole_batch_bench_steps_each_run_the_batch_once(monkeypatch):
+    """--block-steps 0: every bench step (warm-up and timed) runs the whole
+    batch once through a feeder of its own, on a dry-run engine: each step
+    generates exactly the workload's tokens (no step sees another's calls)."""
+    import argparse
+    import torch
+    from moa_inputs import CONFIGS, make_workload
+    bench = _bench()
+    monkeypatch.setattr(torch.cuda, "synchronize", lambda *a, **k: None)
+    cfg = CONFIGS["tiny-moa-fp32"]
+    n_models = cfg.n_experts + (1 if cfg.aggregator else 0)
+    eng, mids = _dry_engine(cfg, n_models)
+    try:
+        args = argparse.Namespace(seed=0, queries=None, gate_tau=None, answer_options=4, order="first-seen",
+                                  window=None, block_steps=0, warmup=2, steps=2, time_every=8)
+        tokens, wall, config, extra, wl = bench.bench_feeder(args, cfg, eng, mids)
+    finally:
+        eng.close()
+    wl = make_workload(cfg.name, 0)
+    per_batch = wl.total_expert_tokens() + wl.n_queries * wl.agg_max_new
+    assert tokens == 2 * per_batch
+    assert config["slice"] == "the whole batch per bench step"
+    assert extra["aggregation"]["aggregator_calls_submitted"] == wl.n_queries
