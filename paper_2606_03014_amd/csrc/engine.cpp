@@ -23,7 +23,7 @@ namespace {
 
 constexpr int kStageSlots = 4;    // steps that may be in flight (pinned staging ring)
 constexpr int kTargetWaves = 4096;
-constexpr int kBigMinRows = 256;    // a row group this large goes to the 32x32-MFMA GEMM
+constexpr int kBigMinRows = 256;    // a row group this large takes the large-M plan (128-row chunks)
 constexpr int kBigTargetWgs = 256;  // one workgroup per CU
 // bf16 steps with several models run them on up to this many streams: the
 // step's models are dealt out in shares of about equal cost (rows laid out
@@ -361,8 +361,8 @@ moa_status resolve_timed(moa_engine* e) {
   } while (0)
 #define LAUNCH(cls, bytes_, flops_, call, what) LAUNCH2(cls, -1, bytes_, flops_, call, what)
 // a GEMM launch: its projection class plus the view of the kernel that runs it
-#define LAUNCH_GEMM(cls, mt_, bytes_, flops_, call, what) \
-  LAUNCH2(cls, (mt_) == kBigTile ? MOA_K_GEMM_LARGE_M : MOA_K_GEMM_SMALL_M, bytes_, flops_, call, what)
+#define LAUNCH_GEMM(cls, large_, bytes_, flops_, call, what) \
+  LAUNCH2(cls, (large_) ? MOA_K_GEMM_LARGE_M : MOA_K_GEMM_SMALL_M, bytes_, flops_, call, what)
 
 // Tile-shuffle a row-major [N][K] bf16 matrix into MFMA B-fragment order:
 // fragment (n/16, k/32) is 64 lanes x 8 contiguous elements, lane = n%16 +
@@ -410,8 +410,9 @@ bool step_is_timed(const moa_engine* e, bool noalloc) {
 
 void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K, int N, int epi, const void* X,
                size_t x_lo, float* out, uint16_t* hout, size_t h_lo, bool allow_split, GemmArgs& a, int& mt,
-               int& nt) {
+               int& nt, bool& large) {
   std::memset(&a, 0, sizeof(a));
+  large = false;
   a.ngroups = ng;
   a.X = X;
   a.x_lo = x_lo;
@@ -436,25 +437,30 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
     return;
   }
   const int KS = K / 32;
-  // Below 256 rows the 128-row tile still wins where its per-workgroup set-up
-  // is amortised over a long k run: square and deep-K projections (N <= K)
-  // from 160 rows, wide ones with K >= 4096 from 192 (cold-weight sweeps of
-  // both model widths, one and four equal groups). Only when every non-empty
-  // group has that many rows: small groups beside one large one would pad
-  // their rows to 128 (one large and three small experts ran 54 us per launch
-  // on 128-row tiles against 42 us on workgroup tiles).
+  // The large-M plan (whole 128-row chunks, split-K only to fill the CUs)
+  // from 256 rows in any group, and below that where every non-empty group
+  // has enough rows for a long k run per workgroup to amortise its set-up:
+  // square and deep-K projections (N <= K) from 160 rows, wide ones with
+  // K >= 4096 from 192 (thresholds from cold-weight sweeps of both model
+  // widths, one and four equal groups, measured with the 128-row tiles).
   const int big_min = N <= K ? 160 : (K >= 4096 ? 192 : kBigMinRows);
   int minM = maxM;
   for (int g = 0; g < in.ngroups; ++g)
     if (in.nrows[g] > 0) minM = std::min(minM, in.nrows[g]);
   if ((maxM >= kBigMinRows || minM >= big_min) && N % 256 == 0) {
-    // matrix-core bound: 128-row tiles on the 32x32 MFMA, split-K only to
-    // give every CU a workgroup
-    mt = kBigTile;
-    nt = (maxM >= 512 && N % 512 == 0) ? 4 : 2;      // 128 x 512 tiles once there are rows for them
-    const int tiles = N / (128 * nt);
+    // matrix-core bound: the medium-M kernel on whole 128-row chunks, 8
+    // waves over 512 columns (256 where N is not a multiple of 512) with a
+    // three-stage weight ring, split-K only to give every CU a workgroup.
+    // Measured against a 32x32-MFMA kernel that staged both operands in LDS
+    // (128 x 512 tiles): 3-29% faster from 512 to 16k rows on 8B shapes, and
+    // more where small groups share the launch (no padded rows multiplied).
+    large = true;
+    const int ct = N % 512 == 0 ? 4 : 2;
+    mt = kMmTile + 8;
+    nt = 16 + ct;
+    const int ncol = N / (128 * ct);
     int base = 0;
-    for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 127) / 128) * tiles;
+    for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 127) / 128) * ncol;
     int S = 1;
     if (allow_split)
       while (base * S < kBigTargetWgs && KS % (S * 2) == 0 && KS / (S * 2) >= 8 &&
@@ -467,9 +473,10 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
     for (int k = 0; k < ng; ++k) {
       const int g = g0 + k;
       a.g[k].W = in.W[g]; a.g[k].row0 = in.row0[g]; a.g[k].nrows = in.nrows[g];
+      a.g[k].mrows = 128;
       a.g[k].n_mc = (in.nrows[g] + 127) / 128;
       a.g[k].item0 = item;
-      item += a.g[k].n_mc * S * tiles;
+      item += a.g[k].n_mc * S * ncol;
     }
     a.total_items = item;
     return;
@@ -532,7 +539,9 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
           T = t;
         }
       mt = kMmTile + sh.rt;
-      nt = sh.nw == 8 ? 8 + sh.ct : sh.ct;
+      // 8 waves: gate-up at RT = 8 with the three-stage weight ring (1-2%
+      // faster there; the F32 projections' shorter k-splits prefer two)
+      nt = sh.nw == 8 ? (epi == EPI_SWIGLU && sh.rt == 8 ? 16 : 8) + sh.ct : sh.ct;
       a.S = S;
       a.ksteps = KS / S;                   // informational: split s takes k-steps [s*KS/S, (s+1)*KS/S)
       a.out_split = (size_t)totalM * N;
@@ -1164,15 +1173,16 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
         const double norm_bytes = (double)b.nr * d * 12.0;
         GemmArgs ga;
         int mt, nt;
+        bool lg;
         LAUNCH(MOA_K_NORM, norm_bytes + b.prev_split * (double)b.nr * d * 4.0, 0,
                launch_add_rmsnorm(st, bf, e->x + ro * d, b.prev_split ? b.part + ro * d : nullptr, b.prev_split,
                                   b.prev_stride, nullptr, sd.row_model + ro, b.nr,
                                   fill([l](const ModelDev& x) { return x.attn_norm[l]; }), xn_b, xn_lo, d,
                                   g.rms_eps), "attn norm");
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wqkv[l]; }), b.g0, b.ng, d, qkv, EPI_F32, e->xn,
-                  xn_lo, b.part, nullptr, 0, true, ga, mt, nt);
+                  xn_lo, b.part, nullptr, 0, true, ga, mt, nt, lg);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH_GEMM(MOA_K_GEMM_QKV, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "qkv gemm");
+        LAUNCH_GEMM(MOA_K_GEMM_QKV, lg, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "qkv gemm");
         LAUNCH(MOA_K_ROPE_KV, (double)b.nr * qkv * 4.0 * ga.S + (double)b.nr * (nh * hd * 4.0 + 2.0 * nkv * hd * esz), 0,
                launch_rope_kv(st, bf, b.part + ro * qkv, ga.S, ga.out_split, sd.row_pos + ro, sd.row_bt + ro,
                               e->bt_store, e->rope, e->q + ro * nh * hd, e->kv, l, e->cfg.num_kv_blocks, nh, nkv, hd,
@@ -1191,29 +1201,29 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
           LAUNCH(MOA_K_ATTN_REDUCE, b.red_bytes, 0,
                  launch_attn_reduce(st, bf, b.red, b.nred, pacc, pml, e->ao, ao_lo, nh, hd), "attn reduce");
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wo[l]; }), b.g0, b.ng, nh * hd, d, EPI_F32, e->ao,
-                  ao_lo, b.part, nullptr, 0, true, ga, mt, nt);
+                  ao_lo, b.part, nullptr, 0, true, ga, mt, nt, lg);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH_GEMM(MOA_K_GEMM_O, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "o gemm");
+        LAUNCH_GEMM(MOA_K_GEMM_O, lg, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "o gemm");
         LAUNCH(MOA_K_NORM, norm_bytes + ga.S * (double)b.nr * d * 4.0, 0,
                launch_add_rmsnorm(st, bf, e->x + ro * d, b.part + ro * d, ga.S, ga.out_split, nullptr,
                                   sd.row_model + ro, b.nr, fill([l](const ModelDev& x) { return x.mlp_norm[l]; }),
                                   xn_b, xn_lo, d, g.rms_eps), "mlp norm");
         if (bf) {
           plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), b.g0, b.ng, d, 2 * F, EPI_SWIGLU,
-                    e->xn, xn_lo, nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt);
+                    e->xn, xn_lo, nullptr, (uint16_t*)e->h, h_lo, false, ga, mt, nt, lg);
           gemm_cost(ga, EPI_SWIGLU, gb, gf);
-          LAUNCH_GEMM(MOA_K_GEMM_GATEUP, mt, gb, gf, launch_gemm(st, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
+          LAUNCH_GEMM(MOA_K_GEMM_GATEUP, lg, gb, gf, launch_gemm(st, bf, ga, EPI_SWIGLU, mt, nt), "gate-up gemm");
         } else {
           plan_gemm(e, weights([l](const ModelDev& x) { return x.wgu[l]; }), b.g0, b.ng, d, 2 * F, EPI_F32, e->xn, 0,
-                    b.part, nullptr, 0, false, ga, mt, nt);
+                    b.part, nullptr, 0, false, ga, mt, nt, lg);
           gemm_cost(ga, EPI_F32, gb, gf);
-          LAUNCH_GEMM(MOA_K_GEMM_GATEUP, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
+          LAUNCH_GEMM(MOA_K_GEMM_GATEUP, lg, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "gate-up gemm");
           HIPCHK(launch_swiglu_f32(st, b.part + ro * 2 * F, (float*)e->h + ro * F, b.nr, F), "swiglu");
         }
         plan_gemm(e, weights([l](const ModelDev& x) { return x.wdown[l]; }), b.g0, b.ng, F, d, EPI_F32, e->h, h_lo,
-                  b.part, nullptr, 0, true, ga, mt, nt);
+                  b.part, nullptr, 0, true, ga, mt, nt, lg);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH_GEMM(MOA_K_GEMM_DOWN, mt, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "down gemm");
+        LAUNCH_GEMM(MOA_K_GEMM_DOWN, lg, gb, gf, launch_gemm(st, bf, ga, EPI_F32, mt, nt), "down gemm");
         b.prev_split = ga.S;
         b.prev_stride = ga.out_split;
       }
@@ -1248,9 +1258,10 @@ moa_status enqueue_step(moa_engine* e, const std::vector<int64_t>& admitted, int
                                   (char*)e->xl + (size_t)b0 * d * L.esz, xl_lo, d, g.rms_eps), "final norm");
         GemmArgs ga;
         int mt, nt;
-        plan_gemm(e, lin, lg0, lng, d, V, EPI_F32, e->xl, xl_lo, e->logits, nullptr, 0, false, ga, mt, nt);
+        bool lg;
+        plan_gemm(e, lin, lg0, lng, d, V, EPI_F32, e->xl, xl_lo, e->logits, nullptr, 0, false, ga, mt, nt, lg);
         gemm_cost(ga, EPI_F32, gb, gf);
-        LAUNCH_GEMM(MOA_K_GEMM_LMHEAD, mt, gb, gf, launch_gemm(b.st, bf, ga, EPI_F32, mt, nt), "lm head");
+        LAUNCH_GEMM(MOA_K_GEMM_LMHEAD, lg, gb, gf, launch_gemm(b.st, bf, ga, EPI_F32, mt, nt), "lm head");
         LAUNCH(MOA_K_ARGMAX, (double)nb * V * 4.0, 0,
                launch_argmax(b.st, e->logits + (size_t)b0 * V, nb, V, sd.lm_dst + b0, e->tok_store), "argmax");
       }

@@ -45,15 +45,12 @@ enum Epilogue { EPI_F32 = 0, EPI_SWIGLU = 1 };
 // launch_gemm(mt = kWgTile + MT, nt = NT): the workgroup-tile kernel; each item
 // is one workgroup of 16*MT rows x 64*NT columns x one k-split (N % (64*NT) == 0).
 constexpr int kWgTile = 1000;
-// launch_gemm(mt = kBigTile, nt = 2 | 4): the large-M kernel on the 32x32
-// MFMA; each item is 128 rows x 128*nt columns x one k-split
-// (N % (128*nt) == 0, K % 32 == 0, ksteps >= 1).
-constexpr int kBigTile = 2000;
 // launch_gemm(mt = kMmTile + RT, nt): the medium-M kernel; each item is 16*RT
 // rows (RT = 2, 4 or 8) x NW*CT*16 columns x one of S k-splits of K/32/S
 // k-steps (rounded; 1 <= S <= K/32), with nt = CT (NW = 4 waves, RT <= 4;
-// CT = 2 or 4) or nt = 8 + CT (NW = 8 waves; CT = 4 with RT >= 4, CT = 2
-// with RT = 8);
+// CT = 2 or 4), nt = 8 + CT (NW = 8 waves; CT = 4 with RT >= 4, CT = 2
+// with RT = 8) or nt = 16 + CT (NW = 8 waves, RT = 8, a three-stage weight
+// register ring; CT = 2 or 4);
 // N must be a multiple of the columns.
 constexpr int kMmTile = 3000;
 

@@ -432,24 +432,10 @@ __global__ __launch_bounds__(256) void k_gemm_wg(GemmArgs a, int nwg) {
   }
 }
 
-// ------------------------------------------------- large-M GEMM (32x32 MFMA)
-// For row groups of a few hundred rows and up (prefill chunks, big decode
-// batches) the GEMM is bound by the matrix cores. v_mfma_f32_32x32x16_bf16
-// sustains about twice the rate of the 16x16x32 form on gfx950, so this path
-// uses it. A workgroup of WM x WN waves computes a (64 WM) x (128 WN) tile;
-// each wave owns 2 x 4 tiles of 32 x 32. Operand layout of the 32x32x16
-// MFMA: A lane l holds row l%32, k = 8 (l/32) .. +8 of a 16-wide k step; B
-// lane l holds column l%32 at the same k; accumulator element e of lane l is
-// row 8 (e/4) + 4 (l/32) + e%4, column l%32.
-//
-// Both operands reach LDS through direct global->LDS loads (no register
-// staging), one 1 KB MFMA fragment per instruction, into a ring of P stages
-// of 32 k each; stage st+P is requested while stage st is consumed, and each
-// wave waits for its own loads with an explicit vmcnt before the workgroup
-// barrier. Activations are read from the split-bf16 planes (both planes of a
-// row tile go through the same B fragment: two MFMAs); weights are read from
-// the tile-shuffled layout, whose 16-column fragments pair up into 32-column
-// MFMA tiles (SwiGLU: a gate tile and the matching up tile side by side).
+// ---------------------------------------- wait, LDS and direct-load helpers
+// Explicit waits, LDS addressing and untracked LDS reads shared by the GEMM
+// and attention kernels below. Direct global->LDS loads
+// (global_load_lds_dwordx4) move one 1 KB MFMA fragment per instruction.
 template <int N> __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
@@ -483,170 +469,6 @@ __device__ __forceinline__ void ds_write_b32(unsigned addr, unsigned v) {
 }
 // Wait for every outstanding LDS access; tying v makes its later uses follow.
 __device__ __forceinline__ void lgkm_wait_for(u32x4& v) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v)); }
-
-template <int WM, int WN, int EPI, int P>
-__global__ __launch_bounds__(64 * WM * WN) void k_gemm_big(GemmArgs a, int nwg) {
-  constexpr int TM = 2, TN = 4;
-  constexpr int NW = WM * WN;
-  constexpr int BM = 32 * TM * WM, BN = 32 * TN * WN;
-  constexpr int FA = (BM / 32) * 4;                   // A fragments per stage: (row tile, plane, k half)
-  constexpr int FB = (BN / 32) * 2;                   // B fragments per stage: (column tile, k half)
-  constexpr int SLOT = (FA + FB) * 1024;
-  constexpr int DPW = (FA + FB) / NW;                 // direct loads per wave per stage
-  static_assert((FA + FB) % NW == 0, "fragments per wave");
-  extern __shared__ __align__(1024) unsigned char smem[];
-  const int per = (nwg + 7) / 8;
-  const int blk = (blockIdx.x % 8) * per + blockIdx.x / 8;
-  if (blk >= a.total_items) return;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int wm = w / WN, wn = w % WN;
-  const void* Wg = a.g[0].W;
-  int row0 = a.g[0].row0, nrows = a.g[0].nrows, n_mc = a.g[0].n_mc, item0 = a.g[0].item0;
-#pragma unroll
-  for (int i = 1; i < kMaxGroups; ++i) {
-    if (i < a.ngroups && a.g[i].item0 <= blk) {
-      Wg = a.g[i].W; row0 = a.g[i].row0; nrows = a.g[i].nrows; n_mc = a.g[i].n_mc; item0 = a.g[i].item0;
-    }
-  }
-  // Item order (workgroups of consecutive ids run at the same time on one
-  // XCD): split by split, then supertiles of up to 4 row tiles x 8 column
-  // tiles, rows fastest, so the ~32 workgroups an XCD holds at once share
-  // their activation and weight stages in its L2.
-  const int idx = blk - item0;
-  const int ncol = a.N / BN;
-  const int s = idx / (n_mc * ncol);
-  const int j = idx - s * n_mc * ncol;
-  const int band = j / (4 * ncol), r0 = band * 4, hb = min(4, n_mc - r0);
-  const int j2 = j - band * 4 * ncol;
-  const int chunk = j2 / (hb * 8), j3 = j2 - chunk * hb * 8;
-  const int mc = r0 + j3 % hb;
-  const int nb = chunk * 8 + j3 / hb;
-  const int ks0 = s * a.ksteps;
-  const int nt0 = nb * (BN / 16);                     // first 16-column weight tile of the block
-  const int KS = a.K >> 5;
-  const int rbase = row0 + mc * BM;
-  const int rend = row0 + nrows;
-  const int c = lane & 31, kh = lane >> 5;
-
-  // per-lane sources of this wave's fragments (fragment w*DPW + i of a stage)
-  const unsigned char* src[DPW];
-  int stride[DPW];
-#pragma unroll
-  for (int i = 0; i < DPW; ++i) {
-    const int f = w * DPW + i;
-    if (f < FA) {
-      const int rt = f >> 2, p = (f >> 1) & 1, h = f & 1;
-      const int r = min(rbase + 32 * rt + c, rend - 1);
-      src[i] = (const unsigned char*)((const uint16_t*)a.X + (size_t)p * a.x_lo + (size_t)r * a.K +
-                                      (size_t)ks0 * 32 + 16 * h + 8 * kh);
-      stride[i] = 64;                                 // bytes per 32-k stage
-    } else {
-      const int g = f - FA, ct = g >> 1, h = g & 1;
-      const int tw = (EPI == EPI_F32) ? nt0 + 2 * ct + (c >> 4) : nt0 + 4 * (ct >> 1) + 2 * (c >> 4) + (ct & 1);
-      src[i] = (const unsigned char*)((const u32x4*)Wg + ((size_t)tw * KS + ks0) * 64 + 16 * (2 * h + kh) + (c & 15));
-      stride[i] = 1024;
-    }
-  }
-  const int nk = a.ksteps;
-  auto issue = [&](int st) {
-    unsigned char* sl = smem + (st % P) * SLOT;
-#pragma unroll
-    for (int i = 0; i < DPW; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)st * stride[i]), MOA_LDS(sl + (w * DPW + i) * 1024),
-                                       16, 0, 0);
-  };
-  // this wave's LDS reads are complete (a wait the compiler sees), then the
-  // workgroup barrier, with no fence that would drain the direct loads
-  auto barrier = [] {
-    wait_lgkm0();
-    asm volatile("s_barrier" ::: "memory");
-  };
-
-  f32x16_t acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
-
-  auto load = [&](int st, int h, u32x4* ra, u32x4* rb) {
-    const unsigned char* sl = smem + (st % P) * SLOT + lane * 16;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int p = 0; p < 2; ++p) ra[i * 2 + p] = *(const u32x4*)(sl + (((wm * TM + i) * 2 + p) * 2 + h) * 1024);
-#pragma unroll
-    for (int j = 0; j < TN; ++j) rb[j] = *(const u32x4*)(sl + (FA + (wn * TN + j) * 2 + h) * 1024);
-  };
-  auto mfmas = [&](const u32x4* ra, const u32x4* rb) {
-#pragma unroll
-    for (int p = 0; p < 2; ++p)
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, ra[i * 2 + p]),
-                                                              __builtin_bit_cast(bf16x8_t, rb[j]), acc[i][j], 0, 0, 0);
-  };
-
-#pragma unroll
-  for (int i = 0; i < P; ++i)
-    if (i < nk) issue(i);
-  if (P <= nk) wait_vmcnt<DPW * (P - 1)>(); else wait_vmcnt<0>();
-  barrier();
-  u32x4 ra0[2 * TM], rb0[TN], ra1[2 * TM], rb1[TN];
-  load(0, 0, ra0, rb0);
-  // stage st: the second k half is read while the first is multiplied; then
-  // stage st+1 is made resident, the slot of stage st refilled with stage
-  // st+P, and the first half of st+1 read while the second half of st is
-  // multiplied. The last stage is peeled so the loop body has no join.
-  for (int st = 0; st + 1 < nk; ++st) {
-    wait_lgkm0();
-    load(st, 1, ra1, rb1);
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas(ra0, rb0);
-    if (st + P <= nk) wait_vmcnt<DPW * (P - 2)>(); else wait_vmcnt<0>();
-    barrier();
-    if (st + P < nk) issue(st + P);
-    load(st + 1, 0, ra0, rb0);
-    __builtin_amdgcn_sched_barrier(0);
-    mfmas(ra1, rb1);
-  }
-  load(nk - 1, 1, ra1, rb1);
-  mfmas(ra0, rb0);
-  mfmas(ra1, rb1);
-
-  const int rw = rbase + wm * TM * 32;
-  if (EPI == EPI_F32) {
-    float* out = a.out + (size_t)s * a.out_split;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int col = nt0 * 16 + (wn * TN + j) * 32 + c;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = rw + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
-          if (r < rend) out[(size_t)r * a.N + col] = acc[i][j][e];
-        }
-      }
-  } else {
-    const int half = a.N >> 1;
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int q = 0; q < TN / 2; ++q) {
-        const int hc = nt0 * 8 + ((wn * TN) / 2 + q) * 32 + c;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = rw + 32 * i + 8 * (e >> 2) + 4 * kh + (e & 3);
-          if (r < rend) {
-            const float g = acc[i][2 * q][e], u = acc[i][2 * q + 1][e];
-            store_split(a.hout, a.h_lo, (size_t)r * half + hc, g / (1.f + __expf(-g)) * u);
-          }
-        }
-      }
-  }
-}
 
 // ------------------------------------------- medium-M GEMM (16x16x32 MFMA)
 // Decode batches put a few dozen to a few hundred rows on each model, so
@@ -1555,22 +1377,6 @@ hipError_t launch_add_rmsnorm(hipStream_t st, bool bf16, float* x, const float* 
   return hipGetLastError();
 }
 
-template <int WM, int WN, int P, int EPI>
-static hipError_t gemm_big(hipStream_t st, const GemmArgs& a) {
-  constexpr int BM = 64 * WM, BN = 128 * WN;
-  constexpr unsigned shm = ((BM / 32) * 4 + (BN / 32) * 2) * 1024 * P;
-  static bool attr = false;                           // one attribute call per instantiation
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute((const void*)k_gemm_big<WM, WN, EPI, P>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)shm);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
-  const int nwg = a.total_items;
-  klaunch_shm(k_gemm_big<WM, WN, EPI, P>, dim3((nwg + 7) / 8 * 8), dim3(64 * WM * WN), shm, st, a, nwg);
-  return hipGetLastError();
-}
-
 template <int RT, int CT, int NW, int D, int EPI>
 static hipError_t gemm_mm(hipStream_t st, const GemmArgs& a) {
   constexpr unsigned shm = 2 * RT * 1024 * (D + 1);
@@ -1586,7 +1392,8 @@ static hipError_t gemm_mm(hipStream_t st, const GemmArgs& a) {
   return hipGetLastError();
 }
 
-// nt: CT (4 waves) or 8 + CT (8 waves); see kMmTile
+// nt: CT (4 waves), 8 + CT (8 waves) or 16 + CT (8 waves, weight ring three
+// stages deep); see kMmTile
 template <int RT, int EPI>
 static hipError_t gemm_mm_nt(hipStream_t st, const GemmArgs& a, int nt) {
   if constexpr (RT <= 4)                          // 4 waves x RT = 8 x CT = 4: one wave per SIMD
@@ -1594,8 +1401,10 @@ static hipError_t gemm_mm_nt(hipStream_t st, const GemmArgs& a, int nt) {
   if (nt == 2) return gemm_mm<RT, 2, 4, 4, EPI>(st, a);
   if constexpr (RT >= 4) {
     if (nt == 12) return gemm_mm<RT, 4, 8, (RT >= 8 ? 2 : 3), EPI>(st, a);
-    if constexpr (RT >= 8)
-      if (nt == 10) return gemm_mm<RT, 2, 8, 3, EPI>(st, a);
+    if constexpr (RT >= 8) {
+      if (nt == 10 || nt == 18) return gemm_mm<RT, 2, 8, 3, EPI>(st, a);
+      if (nt == 20) return gemm_mm<RT, 4, 8, 3, EPI>(st, a);
+    }
   }
   return hipErrorInvalidValue;
 }
@@ -1604,7 +1413,7 @@ hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, in
   if (a.total_items <= 0) return hipSuccess;
   if (bf16 && mt > kMmTile && mt <= kMmTile + 8) {   // medium-M: 16*RT rows x (16 * NW * CT) columns
     const int rt = mt - kMmTile;
-    const int cols = nt > 8 ? 8 * 16 * (nt - 8) : 4 * 16 * nt;
+    const int cols = nt > 16 ? 8 * 16 * (nt - 16) : (nt > 8 ? 8 * 16 * (nt - 8) : 4 * 16 * nt);
     if (a.S < 1 || a.S > (a.K >> 5) || a.N % cols != 0) return hipErrorInvalidValue;
     for (int g = 0; g < a.ngroups; ++g)
       if (a.g[g].mrows < 0 || a.g[g].mrows % 16 != 0 || a.g[g].mrows > 16 * rt) return hipErrorInvalidValue;
@@ -1617,11 +1426,6 @@ hipError_t launch_gemm(hipStream_t st, bool bf16, const GemmArgs& a, int epi, in
       if (rt == 4) return gemm_mm_nt<4, EPI_F32>(st, a, nt);
       if (rt == 8) return gemm_mm_nt<8, EPI_F32>(st, a, nt);
     }
-    return hipErrorInvalidValue;
-  }
-  if (bf16 && mt == kBigTile) {                       // 128 x (128 nt) tiles on the 32x32 MFMA
-    if (nt == 2) return epi == EPI_SWIGLU ? gemm_big<2, 2, 4, EPI_SWIGLU>(st, a) : gemm_big<2, 2, 4, EPI_F32>(st, a);
-    if (nt == 4) return epi == EPI_SWIGLU ? gemm_big<2, 4, 3, EPI_SWIGLU>(st, a) : gemm_big<2, 4, 3, EPI_F32>(st, a);
     return hipErrorInvalidValue;
   }
   if (bf16 && mt >= kWgTile) {
