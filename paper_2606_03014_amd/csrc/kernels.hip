@@ -1190,42 +1190,41 @@ __global__ __launch_bounds__(256) void k_attn_reduce(const ReduceItem* __restric
                                                      const float* __restrict__ pml, void* __restrict__ outv,
                                                      size_t out_lo, int n_h, int hd) {
   // One workgroup per (row, head); G = 256 / hd groups of hd lanes take every
-  // G-th slot, so a row with many key ranges needs G times fewer dependent
-  // load rounds. The slot maximum comes from all 256 lanes at once.
-  __shared__ float sm[4];
+  // G-th slot in one pass, each with its own running maximum (its sums are
+  // rescaled when a slot's maximum exceeds it), so no pass over the slots
+  // waits for another; then the G groups are merged in fixed order.
+  __shared__ float sm[4], sl[4];
   __shared__ float so[256];
-  __shared__ float sl[4];
   const ReduceItem it = red[blockIdx.y];
   const int h = blockIdx.x;
   const int G = 256 / hd;
   const int g = threadIdx.x / hd, dd = threadIdx.x % hd;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  float M = -INFINITY;
-  for (int s = threadIdx.x; s < it.nslots; s += 256) M = fmaxf(M, pml[((size_t)(it.slot0 + s) * n_h + h) * 2]);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 64));
-  if (lane == 0) sm[w] = M;
-  __syncthreads();
-  M = fmaxf(fmaxf(sm[0], sm[1]), fmaxf(sm[2], sm[3]));
-  float L = 0.f, o = 0.f;
-#pragma unroll 8
+  float M = -INFINITY, L = 0.f, o = 0.f;
+#pragma unroll 4
   for (int s = g; s < it.nslots; s += G) {
     const size_t b = (size_t)(it.slot0 + s) * n_h + h;
-    const float wgt = __builtin_amdgcn_exp2f(pml[b * 2] - M);
-    L += pml[b * 2 + 1] * wgt;
-    o += pacc[b * hd + dd] * wgt;
+    const float ms = pml[b * 2], ls = pml[b * 2 + 1], as = pacc[b * hd + dd];
+    const float mn = fmaxf(M, ms);
+    const float wa = __builtin_amdgcn_exp2f(M - mn), wb = __builtin_amdgcn_exp2f(ms - mn);
+    L = L * wa + ls * wb;
+    o = o * wa + as * wb;
+    M = mn;
   }
   so[threadIdx.x] = o;
-  if (dd == 0) sl[g] = L;
+  if (dd == 0) { sm[g] = M; sl[g] = L; }
   __syncthreads();
   if (g == 0) {
-    for (int k = 1; k < G; ++k) {
-      o += so[k * hd + dd];
-      L += sl[k];
+    float Mt = sm[0];
+    for (int k = 1; k < G; ++k) Mt = fmaxf(Mt, sm[k]);
+    float Lt = 0.f, ot = 0.f;
+    for (int k = 0; k < G; ++k) {
+      const float w = __builtin_amdgcn_exp2f(sm[k] - Mt);   // a group without slots: -inf -> 0
+      Lt += sl[k] * w;
+      ot += so[k * hd + dd] * w;
     }
     const size_t oo = ((size_t)it.row * n_h + h) * hd + dd;
-    if (BF) store_split((uint16_t*)outv, out_lo, oo, o / L);
-    else ((float*)outv)[oo] = o / L;
+    if (BF) store_split((uint16_t*)outv, out_lo, oo, ot / Lt);
+    else ((float*)outv)[oo] = ot / Lt;
   }
 }
 
