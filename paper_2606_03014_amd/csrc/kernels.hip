@@ -470,12 +470,16 @@ __device__ __forceinline__ void ds_write_b32(unsigned addr, unsigned v) {
 // Wait for every outstanding LDS access; tying v makes its later uses follow.
 __device__ __forceinline__ void lgkm_wait_for(u32x4& v) { asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(v)); }
 
-// ------------------------------------------- medium-M GEMM (16x16x32 MFMA)
-// Decode batches put a few dozen to a few hundred rows on each model, so
-// every weight byte feeds only that many rows of MFMA work: the GEMM must
-// stream the weights at HBM speed. A workgroup of NW waves owns up to 16*RT
-// rows of one model (all of them, for groups up to that size, so each weight
-// tile leaves HBM once per step) x NW * CT * 16 columns x one k-split.
+// ----------------------------- medium- and large-M GEMM (16x16x32 MFMA)
+// From a few dozen rows per model up to prefill chunks of many thousands.
+// At decode sizes every weight byte feeds only that many rows of MFMA work,
+// so the GEMM must stream the weights at HBM speed; at prefill sizes it is
+// bound by the matrix cores, and keeping the weights out of LDS leaves the
+// LDS to the activations. A workgroup of NW waves owns one row chunk of a
+// group (mrows rows, at most 16*RT: a group of up to that many rows is one
+// chunk, so each weight tile leaves HBM once per step; a larger group is cut
+// into chunks whose items for one column block run side by side on one XCD)
+// x NW * CT * 16 columns x one k-split.
 //  * The split-bf16 activation block of a 32-k stage (2*RT fragments of 1 KB,
 //    both planes) is shared by the waves: it goes HBM/L2 -> LDS by direct
 //    loads into a ring of D + 1 slots.
