@@ -54,23 +54,34 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_code_digest(path):
+    """sha256/16 of a kernel source with its comments and blank lines taken
+    out, so that a counter record stays valid across edits to comments only
+    (the compiled kernels are the same) and lapses with any change to code."""
+    import hashlib
+    import re
+    src = open(path, encoding="utf-8").read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    lines = [ln.rstrip() for ln in src.splitlines() if ln.strip()]
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()[:16]
+
+
 def measured_traffic(kernel, workload, streams=1):
     """HBM bytes per launch of ``kernel`` on ``workload`` from the committed
     rocprofv3 counter summaries, or None when none exists, the kernel source
-    changed since, or the counters were taken with another number of model
-    streams (which changes what one launch carries). The roofline's launches
+    code changed since (kernel_code_digest), or the counters were taken with
+    another number of model streams (which changes what one launch carries). The roofline's launches
     are those of the steps sampled for timing, which always run on one
     stream, so it asks for the one-stream counters."""
     import glob
-    import hashlib
-    src = os.path.join(ROOT, "paper_2606_03014_amd", "csrc", "kernels.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    sha = kernel_code_digest(os.path.join(ROOT, "paper_2606_03014_amd", "csrc", "kernels.hip"))
     for path in glob.glob(os.path.join(ROOT, "profiles", "*traffic*.md")):
         for line in open(path):
             line = line.strip()
             if line.startswith("{") and '"traffic_bytes_per_launch"' in line:
                 rec = json.loads(line)
-                if (rec.get("kernel") == kernel and rec.get("kernels_source_sha256_16") == sha
+                if (rec.get("kernel") == kernel and rec.get("kernels_code_sha256_16") == sha
                         and rec.get("workload") == workload and rec.get("model_streams", 1) == streams):
                     return rec["traffic_bytes_per_launch"]
     return None

@@ -1,5 +1,4 @@
 """bench.py's reading of committed counter records (CPU only)."""
-import hashlib
 import importlib.util
 import json
 import os
@@ -21,16 +20,16 @@ def test_traffic_records_match_source_workload_and_streams(tmp_path):
     bench = _bench()
     src = tmp_path / "paper_2606_03014_amd" / "csrc"
     src.mkdir(parents=True)
-    (src / "kernels.hip").write_bytes(b"// kernels\n")
-    sha = hashlib.sha256(b"// kernels\n").hexdigest()[:16]
+    (src / "kernels.hip").write_text("// kernels\nint k;  // one\n/* block\n comment */\n")
+    sha = bench.kernel_code_digest(str(src / "kernels.hip"))
     prof = tmp_path / "profiles"
     prof.mkdir()
     recs = [
-        {"kernel": "gemm_gateup", "kernels_source_sha256_16": sha, "workload": "w", "model_streams": 2,
+        {"kernel": "gemm_gateup", "kernels_code_sha256_16": sha, "workload": "w", "model_streams": 2,
          "traffic_bytes_per_launch": 2.0},
-        {"kernel": "gemm_gateup", "kernels_source_sha256_16": sha, "workload": "w",
+        {"kernel": "gemm_gateup", "kernels_code_sha256_16": sha, "workload": "w",
          "traffic_bytes_per_launch": 1.0},
-        {"kernel": "attn", "kernels_source_sha256_16": "0" * 16, "workload": "w", "model_streams": 1,
+        {"kernel": "attn", "kernels_code_sha256_16": "0" * 16, "workload": "w", "model_streams": 1,
          "traffic_bytes_per_launch": 3.0},
     ]
     (prof / "traffic_w.md").write_text("# t\n\n```\n" + "\n".join(json.dumps(r) for r in recs) + "\n```\n")
@@ -41,6 +40,11 @@ def test_traffic_records_match_source_workload_and_streams(tmp_path):
     assert bench.measured_traffic("gemm_gateup", "other", 2) is None
     assert bench.measured_traffic("attn", "w", 1) is None          # another kernel source
     assert bench.measured_traffic("gemm_down", "w", 1) is None
+    # comments and blank lines do not change the digest; code does
+    (src / "kernels.hip").write_text("// other words\n\nint k;   /* note */\n")
+    assert bench.measured_traffic("gemm_gateup", "w", 1) == 1.0
+    (src / "kernels.hip").write_text("int k2;\n")
+    assert bench.measured_traffic("gemm_gateup", "w", 1) is None
 
 
 def test_bench_refuses_more_than_one_gpu():
