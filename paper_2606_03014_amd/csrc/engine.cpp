@@ -482,18 +482,22 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
     return;
   }
   // Medium row counts (17 and up per model, below the large-M thresholds):
-  // the medium-M kernel, whole 16-row tiles of a group per workgroup
-  // (RT tiles: 2 up to 32 rows, 4 up to 64, else 8 per row chunk), 8 waves
-  // over 512 columns where N allows (otherwise 8 waves over 256 at RT = 8,
-  // 4 waves over 256 below: a vocabulary of 128,256 is 501 x 256, and two
-  // 64-row chunks per model would stream its LM head twice), and about one
-  // workgroup per CU: F32 projections take
-  // the k-split that brings the grid nearest ~224 workgroups; gate-up (no
-  // k-split: its SwiGLU epilogue needs the whole sum) the first tile shape
-  // whose grid has 150..256 workgroups, else the workgroup-tile kernel.
+  // the medium-M kernel.
+  //  * Whole 16-row tiles of a group per workgroup: RT tiles per row chunk,
+  //    2 up to 32 rows, 4 up to 64, else 8.
+  //  * 8 waves over 512 columns where N allows; otherwise 8 waves over 256
+  //    at RT = 8 and 4 waves over 256 below (a vocabulary of 128,256 is
+  //    501 x 256, and two 64-row chunks per model would stream its LM head
+  //    twice).
+  //  * About one workgroup per CU. F32 projections take the k-split that
+  //    brings the grid nearest ~224 workgroups; gate-up (no k-split: its
+  //    SwiGLU epilogue needs the whole sum) takes the first tile shape whose
+  //    grid has 150..256 workgroups, else the workgroup-tile kernel.
   // Measured on 8B shapes with cold weights, three groups of 16..200 rows:
   // 2-40% faster per projection than the workgroup-tile kernel, and
-  // bit-identical on the same split.
+  // bit-identical on the same split. A 4-wave, 64-row-chunk plan with
+  // three k-splits for the square O projection (its norm then reads fewer
+  // partials) measured no faster in the 3+1x8B window.
   if (maxM > 16 && N % 256 == 0) {
     struct Shape { int rt, nw, ct; };
     auto chunks_of = [&](int rt) {
