@@ -6,8 +6,12 @@ documented error return) is compiled with both sanitizers on its host side
 and linked, with the normally built kernel objects, into a small C program
 that drives MOA_FLAG_PLAN_ONLY engines through the C ABI
 (tests/sanitize/plan_driver.c). A plan-only engine makes no HIP call, so this
-runs without a GPU. The oracle is Python (numpy) and has no native code to
-sanitize.
+runs without a GPU. The grouped-GEMM planner, which only runs when a step is
+enqueued on a GPU, is checked on its own by tests/sanitize/gemm_plan_check.cpp
+(it includes engine.cpp): random ragged row mixes on the 8B, 1B and a small
+model's projections, every plan replayed through the kernels' item decode for
+exact coverage, launchability and partial-buffer bounds, under the same two
+sanitizers. The oracle is Python (numpy) and has no native code to sanitize.
 """
 import os
 import shutil
@@ -29,23 +33,42 @@ def _run(cmd, **kw):
     return r
 
 
-@pytest.fixture(scope="module")
-def driver(tmp_path_factory):
+def _kernel_objs():
     if not (os.path.exists(HIPCC) and os.path.exists(os.path.join(LLVM, "clang"))):
         pytest.skip("ROCm toolchain not found")
-    from paper_2606_03014_amd.build import FLAGS, build
+    from paper_2606_03014_amd.build import build
     objs = [os.path.join(BUILD, s + ".o") for s in ("kernels.hip", "peaks.hip")]
     if not all(os.path.exists(o) for o in objs):
         build()
-    out = tmp_path_factory.mktemp("san")
+    return objs
+
+
+def _hipcc_san(src, obj):
+    """Compile one host translation unit with both sanitizers on its host side."""
+    from paper_2606_03014_amd.build import FLAGS
     host_san = []
     for s in SAN:          # sanitizers on the host side only
         host_san += ["-Xarch_host", f"-fsanitize={s}"]
-    eng_o = str(out / "engine_san.o")
     flags = [f for f in FLAGS if f != "-O3"]
     _run([HIPCC] + flags + ["-O1", "-g", "-Xarch_host", "-fno-omit-frame-pointer",
-                            "-Xarch_host", "-fno-sanitize-recover=all"] + host_san +
-         ["-c", os.path.join(CSRC, "engine.cpp"), "-o", eng_o])
+                            "-Xarch_host", "-fno-sanitize-recover=all"] + host_san + ["-c", src, "-o", obj])
+
+
+def _san_env():
+    env = dict(os.environ)
+    env["ASAN_OPTIONS"] = "detect_leaks=1:abort_on_error=0:halt_on_error=1"
+    env["UBSAN_OPTIONS"] = "print_stacktrace=1:halt_on_error=1"
+    supp = os.path.join(ROOT, "tests", "sanitize", "lsan.supp")
+    env["LSAN_OPTIONS"] = f"suppressions={supp}"
+    return env
+
+
+@pytest.fixture(scope="module")
+def driver(tmp_path_factory):
+    objs = _kernel_objs()
+    out = tmp_path_factory.mktemp("san")
+    eng_o = str(out / "engine_san.o")
+    _hipcc_san(os.path.join(CSRC, "engine.cpp"), eng_o)
     drv_o = str(out / "plan_driver.o")
     san = ",".join(SAN)
     _run([os.path.join(LLVM, "clang"), "-std=c11", "-O1", "-g", "-Wall", f"-fsanitize={san}",
@@ -58,13 +81,31 @@ def driver(tmp_path_factory):
 
 
 def test_plan_only_engine_is_clean_under_asan_and_ubsan(driver):
-    env = dict(os.environ)
-    env["ASAN_OPTIONS"] = "detect_leaks=1:abort_on_error=0:halt_on_error=1"
-    env["UBSAN_OPTIONS"] = "print_stacktrace=1:halt_on_error=1"
-    supp = os.path.join(ROOT, "tests", "sanitize", "lsan.supp")
-    env["LSAN_OPTIONS"] = f"suppressions={supp}"
-    r = subprocess.run([driver], capture_output=True, text=True, env=env, timeout=300)
+    r = subprocess.run([driver], capture_output=True, text=True, env=_san_env(), timeout=300)
     log = r.stdout + r.stderr
     assert r.returncode == 0, log[-6000:]
     assert "ERROR: AddressSanitizer" not in log and "runtime error" not in log, log[-6000:]
     assert "plan_driver: ok" in r.stdout
+
+
+@pytest.fixture(scope="module")
+def plan_check(tmp_path_factory):
+    objs = _kernel_objs()
+    out = tmp_path_factory.mktemp("plan")
+    obj = str(out / "gemm_plan_check.o")
+    _hipcc_san(os.path.join(ROOT, "tests", "sanitize", "gemm_plan_check.cpp"), obj)
+    san = ",".join(SAN)
+    exe = str(out / "gemm_plan_check")
+    _run([os.path.join(LLVM, "clang++"), f"-fsanitize={san}", obj] + objs +
+         ["-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib", "-o", exe])
+    return exe
+
+
+def test_gemm_plans_cover_every_output_once_and_launch(plan_check):
+    # 120 random steps per (dtype, model shape): about 3,500 plans, every
+    # share launch replayed item by item
+    r = subprocess.run([plan_check, "120"], capture_output=True, text=True, env=_san_env(), timeout=300)
+    log = r.stdout + r.stderr
+    assert r.returncode == 0, log[-6000:]
+    assert "ERROR: AddressSanitizer" not in log and "runtime error" not in log, log[-6000:]
+    assert "gemm_plan_check: ok" in r.stdout
