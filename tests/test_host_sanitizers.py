@@ -11,7 +11,11 @@ enqueued on a GPU, is checked on its own by tests/sanitize/gemm_plan_check.cpp
 (it includes engine.cpp): random ragged row mixes on the 8B, 1B and a small
 model's projections, every plan replayed through the kernels' item decode for
 exact coverage, launchability and partial-buffer bounds, under the same two
-sanitizers. The oracle is Python (numpy) and has no native code to sanitize.
+sanitizers. tests/sanitize/step_plan_check.cpp checks every step's attention,
+combine, prefill-block and LM-row lists of plan-only engines against the
+request bookkeeping (keys covered once per row, partial slots, block-list
+offsets, tokens read only once written, share order). The oracle is Python
+(numpy) and has no native code to sanitize.
 """
 import os
 import shutil
@@ -88,24 +92,47 @@ def test_plan_only_engine_is_clean_under_asan_and_ubsan(driver):
     assert "plan_driver: ok" in r.stdout
 
 
-@pytest.fixture(scope="module")
-def plan_check(tmp_path_factory):
+def _check_program(tmp_path_factory, name):
+    """Build tests/sanitize/<name>.cpp (it includes engine.cpp) with both sanitizers."""
     objs = _kernel_objs()
-    out = tmp_path_factory.mktemp("plan")
-    obj = str(out / "gemm_plan_check.o")
-    _hipcc_san(os.path.join(ROOT, "tests", "sanitize", "gemm_plan_check.cpp"), obj)
+    out = tmp_path_factory.mktemp(name)
+    obj = str(out / (name + ".o"))
+    _hipcc_san(os.path.join(ROOT, "tests", "sanitize", name + ".cpp"), obj)
     san = ",".join(SAN)
-    exe = str(out / "gemm_plan_check")
+    exe = str(out / name)
     _run([os.path.join(LLVM, "clang++"), f"-fsanitize={san}", obj] + objs +
          ["-L/opt/rocm/lib", "-lamdhip64", "-Wl,-rpath,/opt/rocm/lib", "-o", exe])
     return exe
 
 
-def test_gemm_plans_cover_every_output_once_and_launch(plan_check):
-    # 120 random steps per (dtype, model shape): about 3,500 plans, every
-    # share launch replayed item by item
-    r = subprocess.run([plan_check, "120"], capture_output=True, text=True, env=_san_env(), timeout=300)
+def _run_check(exe, arg, name):
+    r = subprocess.run([exe, arg], capture_output=True, text=True, env=_san_env(), timeout=300)
     log = r.stdout + r.stderr
     assert r.returncode == 0, log[-6000:]
     assert "ERROR: AddressSanitizer" not in log and "runtime error" not in log, log[-6000:]
-    assert "gemm_plan_check: ok" in r.stdout
+    assert f"{name}: ok" in r.stdout
+    return r.stdout
+
+
+@pytest.fixture(scope="module")
+def plan_check(tmp_path_factory):
+    return _check_program(tmp_path_factory, "gemm_plan_check")
+
+
+@pytest.fixture(scope="module")
+def step_check(tmp_path_factory):
+    return _check_program(tmp_path_factory, "step_plan_check")
+
+
+def test_gemm_plans_cover_every_output_once_and_launch(plan_check):
+    # 120 random steps per (dtype, model shape): about 3,500 plans, every
+    # share launch replayed item by item
+    _run_check(plan_check, "120", "gemm_plan_check")
+
+
+def test_step_work_lists_cover_every_key_once_in_causal_order(step_check):
+    # four plan-only engines (f32; bf16 at head_dim 64 and 128 on model
+    # streams; bf16 on one stream), 300 requests each with histories up to
+    # 33k positions: every step's attention, combine, prefill and LM lists
+    out = _run_check(step_check, "300", "step_plan_check")
+    assert out.count("split rows") == 4
