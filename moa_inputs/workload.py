@@ -10,7 +10,7 @@ heavier-tailed outputs than instruction-style ones (Observation 1).
 Each quantity has its own stream keyed by (seed, workload id, stream id), so a
 change in one draw never shifts another.
 """
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 import numpy as np
 
 from .configs import CONFIGS

@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 
 from moa_inputs import CONFIGS, generate_weights, make_workload, pack_blob, f32_to_bf16_bits
-from moa_inputs.configs import EngineConsts, LLAMA_8B
+from moa_inputs.configs import EngineConsts
 from moa_inputs.workload import synthetic_kv
 from oracle import transformer as T
 from paper_2606_03014_amd import Engine

@@ -18,7 +18,6 @@ offsets, tokens read only once written, share order). The oracle is Python
 (numpy) and has no native code to sanitize.
 """
 import os
-import shutil
 import subprocess
 
 import pytest

@@ -1,6 +1,4 @@
 """Pins for the oracle's whole-model paths (forward, caches, greedy decoding)."""
-from dataclasses import replace
-
 import numpy as np
 import pytest
 
