@@ -25,6 +25,12 @@ constexpr int kStageSlots = 4;    // steps that may be in flight (pinned staging
 constexpr int kTargetWaves = 4096;
 constexpr int kBigMinRows = 256;    // a row group this large takes the large-M plan (128-row chunks)
 constexpr int kBigTargetWgs = 256;  // one workgroup per CU
+// Large-M k-split cost, fitted to cold-weight sweeps of the 8B projections
+// (300 to 4,096 rows in one to four groups, S = 1..8; 4.6% rms): per
+// 32-wide k-step of a workgroup, each round of the grid over the CUs costs
+// kRoundUs and the grid's size in CU-fulls kGridUs; every byte of partial
+// sums costs kPartialUs to write and, in the consumer, to read back.
+constexpr double kRoundUs = 1.075, kGridUs = 0.442, kPartialUs = 0.37e-6;
 // bf16 steps with several models run them on up to this many streams: the
 // step's models are dealt out in shares of about equal cost (rows laid out
 // share by share), the first on the caller's stream, the others on streams
@@ -450,7 +456,7 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
   if ((maxM >= kBigMinRows || minM >= big_min) && N % 256 == 0) {
     // matrix-core bound: the medium-M kernel on whole 128-row chunks, 8
     // waves over 512 columns (256 where N is not a multiple of 512) with a
-    // three-stage weight ring, split-K only to give every CU a workgroup.
+    // three-stage weight ring.
     // Measured against a 32x32-MFMA kernel that staged both operands in LDS
     // (128 x 512 tiles): 3-29% faster from 512 to 16k rows on 8B shapes, and
     // more where small groups share the launch (no padded rows multiplied).
@@ -461,13 +467,26 @@ void plan_gemm(const moa_engine* e, const GemmPlanIn& in, int g0, int ng, int K,
     const int ncol = N / (128 * ct);
     int base = 0;
     for (int g = 0; g < in.ngroups; ++g) base += ((in.nrows[g] + 127) / 128) * ncol;
+    // k-split (any S; at least 8 k-steps each) at the least fitted cost: a
+    // grid just past the CUs runs a second, nearly empty round, and every
+    // split adds partial sums. Against a power-of-two split grown until the
+    // grid covered the CUs, measured with the consumer's read: o and down
+    // 15-30% faster at 300-2,200 rows in several groups (S = 3..7 where
+    // that gave 2 or 4), qkv 7-28% (S = 1 or 2 against 2 or 4; 5 against 8
+    // at 512 rows in one group).
     int S = 1;
-    if (allow_split)
-      while (base * S < kBigTargetWgs && KS % (S * 2) == 0 && KS / (S * 2) >= 8 &&
-             (int64_t)S * 2 * totalM * N <= e->lay.part_cap && S < 16)
-        S *= 2;
+    if (allow_split) {
+      double best = 0;
+      for (int s = 1; s <= 16 && KS / s >= 8; ++s) {
+        if ((int64_t)s * totalM * N > e->lay.part_cap) break;
+        const double items = (double)base * s;
+        const double cost = (kRoundUs * std::ceil(items / kBigTargetWgs) + kGridUs * items / kBigTargetWgs) * KS / s +
+                            kPartialUs * 4.0 * s * (double)totalM * N;
+        if (s == 1 || cost < best) { best = cost; S = s; }
+      }
+    }
     a.S = S;
-    a.ksteps = KS / S;
+    a.ksteps = KS / S;                     // informational: split s takes k-steps [s*KS/S, (s+1)*KS/S)
     a.out_split = (size_t)totalM * N;
     int item = 0;
     for (int k = 0; k < ng; ++k) {
