@@ -210,6 +210,7 @@ int rows_draw(int cap) {
 
 int main(int argc, char** argv) {
   const int cases = argc > 1 ? std::atoi(argv[1]) : 400;
+  if (argc > 2) g_rng ^= std::strtoull(argv[2], nullptr, 10) * 0x9e3779b97f4a7c15ull;   // another seed
   const Shape shapes[3] = {
       {"8B", {32, 4096, 32, 8, 128, 14336, 128256, 500000.f, 1e-5f}},
       {"1B", {16, 2048, 32, 8, 64, 8192, 128256, 500000.f, 1e-5f}},

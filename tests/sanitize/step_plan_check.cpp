@@ -324,6 +324,7 @@ void run(int32_t dtype, int32_t hd, int32_t flags, int n_req) {
 
 int main(int argc, char** argv) {
   const int n_req = argc > 1 ? std::atoi(argv[1]) : 300;
+  if (argc > 2) g_rng ^= std::strtoull(argv[2], nullptr, 10) * 0x9e3779b97f4a7c15ull;   // another seed
   run(MOA_F32, 64, 0, n_req);
   run(MOA_BF16, 64, 0, n_req);
   run(MOA_BF16, 128, 0, n_req);
