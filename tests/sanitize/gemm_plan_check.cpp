@@ -15,7 +15,8 @@
 //   * a share's launch picks the same tiling, split and partial stride as the
 //     whole step, so its partials land where the step's consumer reads them;
 //   * gate-up (SwiGLU epilogue) is never split and, on the medium-M kernel,
-//     fits one workgroup per CU.
+//     fits one workgroup per CU;
+//   * the large-M k-split still picks the splits measured best on the GPU.
 // The decode below restates the kernels' index arithmetic: a change to either
 // side that breaks the contract fails here, on the CPU. No HIP call is made.
 #include "../../paper_2606_03014_amd/csrc/engine.cpp"
@@ -195,6 +196,43 @@ bool check_case(const moa_engine& e, const Proj& p, const GemmPlanIn& in, const 
   return true;
 }
 
+// Large-M k-splits measured best on an MI355X (cold 8B weights, the GEMM
+// plus its consumer's read of the partials), at the workspace of a
+// 16,384-token prefill budget and 512 sequences: the fitted cost must keep
+// choosing them.
+bool measured_splits() {
+  moa_engine_cfg cfg{};
+  cfg.model = {32, 4096, 32, 8, 128, 14336, 128256, 500000.f, 1e-5f};
+  cfg.dtype = MOA_BF16; cfg.kv_block_size = kBlock; cfg.num_kv_blocks = 4096; cfg.max_num_seqs = 512;
+  cfg.max_prefill_tokens = 16384; cfg.max_model_len = 40000; cfg.max_models = 4;
+  moa_engine e;
+  e.cfg = cfg;
+  e.bf16 = true;
+  e.lay = make_layout(cfg);
+  struct Case { const char* name; int K, N; std::vector<int> rows; int S; };
+  const Case cases[] = {
+      {"qkv", 4096, 6144, {512}, 5},          {"qkv", 4096, 6144, {300}, 7},
+      {"qkv", 4096, 6144, {2048, 90, 80}, 1}, {"qkv", 4096, 6144, {700, 80, 90, 60}, 2},
+      {"o", 4096, 4096, {2048, 90, 80}, 3},   {"o", 4096, 4096, {2600}, 3},
+      {"o", 4096, 4096, {300}, 9},            {"o", 4096, 4096, {16384}, 1},
+      {"down", 14336, 4096, {2048, 90, 80}, 5}, {"down", 14336, 4096, {300}, 10},
+      {"down", 14336, 4096, {8000, 100, 90}, 3}, {"down", 14336, 4096, {16384}, 1},
+  };
+  for (const Case& c : cases) {
+    GemmPlanIn in;
+    in.ngroups = (int)c.rows.size();
+    int row = 0;
+    for (int g = 0; g < in.ngroups; ++g) { in.row0[g] = row; in.nrows[g] = c.rows[g]; row += c.rows[g]; in.W[g] = nullptr; }
+    GemmArgs a;
+    int mt = 0, nt = 0;
+    bool large = false;
+    plan_gemm(&e, in, 0, in.ngroups, c.K, c.N, EPI_F32, nullptr, 0, nullptr, nullptr, 0, true, a, mt, nt, large);
+    CHECK(large && a.S == c.S, "%s at %d rows in %d groups: large %d S %d, measured best S %d", c.name, row, in.ngroups,
+          large, a.S, c.S);
+  }
+  return true;
+}
+
 int rows_draw(int cap) {
   switch (rnd(6)) {
     case 0: return 0;
@@ -219,6 +257,7 @@ int main(int argc, char** argv) {
   const int prefill_caps[4] = {512, 2048, 8192, 16384};
   const int seq_caps[3] = {64, 256, 512};
   long planned = 0;
+  if (!measured_splits()) return 1;
   for (int dt = 0; dt < 2; ++dt)
     for (const Shape& sh : shapes)
       for (int c = 0; c < cases; ++c) {
