@@ -380,14 +380,17 @@ def test_bf16_injected_history_pareto_lengths():
 @pytest.mark.parametrize("n", [100, 180, 300, 520], ids=["100-rows", "180-rows", "300-rows", "520-rows"])
 def test_bf16_wide_decode_batch(n):
     """A decode batch of n rows of one 8B-width model (two layers): every
-    projection and the LM head run as one n-row group. 300 rows take the
-    large-M 32x32-MFMA GEMM (the shape of the straggler workload's refill
-    phase), 100 rows the workgroup-tile kernel with its widest tiles (64 rows
-    x 256 columns), 180 rows both: the square and deep-K projections (o,
-    down) on 128-row tiles with a partly empty second tile, the wide ones
-    (qkv, gate-up, LM head) on workgroup tiles. 520 rows take the
-    128x512 tiles of the large-M GEMM with a partly empty last row tile. Eight of the calls carry a host K/V history and are
-    checked teacher-forced against the oracle; the rest have device-filled
+    projection and the LM head run as one n-row group.
+    * 100 rows: every projection on the medium-row plan (one 112-row chunk,
+      16 k-splits for qkv, o and down).
+    * 180 rows: o and down on the large-row plan (two 128-row chunks, the
+      second partly empty; 11 and 16 k-splits), qkv, gate-up and the LM head
+      on the medium-row plan.
+    * 300 and 520 rows (the straggler workload's refill phase): everything
+      on the large-row plan, with uneven k-splits (7/9/10 and 4/6/6 for
+      qkv/o/down) and a partly empty last chunk.
+    Eight of the calls carry a host K/V history and are checked
+    teacher-forced against the oracle; the rest have device-filled
     histories and only set the batch shape."""
     from moa_inputs import f32_to_bf16_bits
     from moa_inputs.workload import synthetic_kv
