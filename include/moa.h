@@ -244,7 +244,11 @@ moa_status moa_debug_chunks(moa_engine* e, int64_t request_id, int64_t* out, int
                             int32_t* n_out);
 
 /* Per-step bookkeeping rows (step, admitted, prefill_tokens, decode_rows,
- * finished, free_blocks_after), 6 int64 per step, oldest first. */
+ * finished, free_blocks_after), 6 int64 per step, oldest first, into out
+ * (caller-owned, cap_steps rows). *n_out is always set to the number of
+ * steps recorded; MOA_EINVAL without writing when cap_steps is smaller (a
+ * call with out = NULL and cap_steps = 0 asks for the count) or when e or
+ * n_out is NULL. */
 moa_status moa_debug_steps(moa_engine* e, int64_t* out, int64_t cap_steps, int64_t* n_out);
 
 /* How the last moa_step split its models over the model streams (a

@@ -249,7 +249,9 @@ def moa_debug_steps(eng):
     import numpy as np
     n = C.c_int64()
     L = lib()
-    code = L.moa_debug_steps(eng, None, 0, C.byref(n))
+    code = L.moa_debug_steps(eng, None, 0, C.byref(n))   # the count (MOA_EINVAL once there are steps)
+    if code not in (MOA_OK, MOA_EINVAL) or (code == MOA_EINVAL and n.value == 0):
+        raise MoaError(code, "moa_debug_steps")
     if n.value == 0:
         return np.zeros((0, 6), dtype=np.int64)
     buf = np.zeros(6 * n.value, dtype=np.int64)
