@@ -93,3 +93,57 @@ def test_whole_batch_bench_steps_each_run_the_batch_once(monkeypatch):
     assert tokens == 2 * per_batch
     assert config["slice"] == "the whole batch per bench step"
     assert extra["aggregation"]["aggregator_calls_submitted"] == wl.n_queries
+
+
+def test_bench_line_keeps_its_contract(monkeypatch, capsys):
+    """The one JSON line bench.py prints, end to end on the CPU: a plan-only
+    engine runs the tiny fp32 workload's schedule (the GPU-only calls, peak
+    probes and kernel timing, are stubbed with fixed figures), and the CPU
+    oracle leg runs for real. Every key the line promises is there, with the
+    right type, and the roofline object is the dominant class's."""
+    import sys
+    import torch
+    import paper_2606_03014_amd as pkg
+    from paper_2606_03014_amd.moa import KERNEL_CLASSES
+    bench = _bench()
+    real_engine = pkg.Engine
+
+    def plan_only_engine(shape, dtype, consts, max_models, **kw):
+        kw.pop("plan_only", None)
+        eng = real_engine(shape, dtype, consts, max_models, plan_only=True, **kw)
+        eng.measure_peaks = lambda: (6.3e12, 2.0e15)
+        # attention dominates the timed kernel time: 4 launches of 2 GB in 1 ms each
+        stats = {n: {"launches": 0, "ms": 0.0, "bytes": 0.0, "flops": 0.0, "launches_all": 0,
+                     "bytes_all": 0.0, "flops_all": 0.0, "roof_ms_all": 0.0} for n in KERNEL_CLASSES}
+        stats["attn"].update(launches=4, ms=4.0, bytes=8e9, flops=1e9, launches_all=4, bytes_all=8e9,
+                             flops_all=1e9, roof_ms_all=1.0)
+        stats["gemm_qkv"].update(launches=4, ms=1.0, bytes=2e9, flops=4e11, launches_all=4, bytes_all=2e9,
+                                 flops_all=4e11, roof_ms_all=0.25)
+        eng.kernel_stats = lambda: stats
+        return eng
+
+    monkeypatch.setattr(pkg, "Engine", plan_only_engine)
+    monkeypatch.setattr(torch.cuda, "synchronize", lambda *a, **k: None)
+    monkeypatch.setattr(torch.cuda, "empty_cache", lambda *a, **k: None)
+    monkeypatch.setattr(sys, "argv", ["bench.py", "--workload", "tiny-moa-fp32", "--steps", "2", "--warmup", "1",
+                                      "--block-steps", "4"])
+    bench.main()
+    lines = [l for l in capsys.readouterr().out.splitlines() if l.strip()]
+    assert len(lines) == 1
+    d = json.loads(lines[0])
+    for k, t in (("metric", str), ("value", float), ("unit", str), ("n_gpus", int), ("steps", int),
+                 ("warmup", int), ("ms_per_step", float), ("higher_is_better", bool), ("scaling", str),
+                 ("dtype", str), ("data", str), ("config", dict), ("roofline", dict), ("cpu_baseline", dict)):
+        assert isinstance(d[k], t), k
+    assert d["n_gpus"] == 1 and d["steps"] == 2 and d["warmup"] == 1 and d["value"] > 0
+    assert d["higher_is_better"] is True and d["scaling"] in ("weak", "strong") and d["vs_baseline"] is None
+    assert d["data"] == "synthetic" and d["config"]["workload"] == "tiny-moa-fp32"
+    assert abs(d["ms_per_step"] * d["steps"] / 1e3 - d["timed_wall_s"]) < 1e-9
+    r = d["roofline"]
+    assert {"bound", "achieved", "peak", "unit", "frac", "traffic"} <= set(r)
+    assert r["kernel"] == "attn" and r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert abs(r["achieved"] - 2000.0) < 1e-6 and abs(r["frac"] - 0.25) < 1e-9
+    assert r["traffic"] is None                      # no counter record for this workload
+    c = d["cpu_baseline"]
+    assert c["kind"] == "oracle" and c["unit"] == "tokens/s" and c["value"] > 0
+    assert isinstance(c["cores"], int) and c["cores"] >= 1 and isinstance(c["sample"], str)
