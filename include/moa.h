@@ -221,7 +221,12 @@ moa_status moa_collect(moa_engine* e, int64_t upto_step, moa_result* res, int32_
 /* Wait for every enqueued step. */
 moa_status moa_sync(moa_engine* e);
 
+/* Wait for the engine's streams, then free what the engine allocated
+ * (host state, pinned staging, streams and events). The device arena stays
+ * the caller's: free it after this returns. NULL is a no-op. */
 void moa_destroy(moa_engine* e);
+/* Static description of a status code ("MOA_OK", "MOA_EINVAL: invalid
+ * argument", ...); never NULL. */
 const char* moa_status_str(moa_status s);
 
 /* ---- inspection hooks (tests) ---- */
